@@ -1,0 +1,131 @@
+"""ctypes front end of the CPU oracle (oracle/oracle.c).
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by the package smoke check and
+by the CPU-baseline leg of bench.py, never by the product path.  It shares no
+code with the HIP sources.  Every function follows FlashDrive Sec. 3.4
+(4-bit weights, 8-bit activations, integer contraction) with the readings
+stated in oracle.c's header.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+GCC_FLAGS = ["-O2", "-ffp-contract=off", "-std=c11", "-fPIC", "-shared", "-pthread"]
+
+OK, EINVAL, ENONFINITE, EOVERFLOW = 0, 1, 2, 3
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c into liboracle.so with gcc (no HIP involved)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.run(["gcc", *GCC_FLAGS, _SRC, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        L = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        I64 = ctypes.c_int64
+        L.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
+        L.oracle_bf16_to_f32.restype = ctypes.c_float
+        L.oracle_f32_to_bf16.argtypes = [ctypes.c_float]
+        L.oracle_f32_to_bf16.restype = ctypes.c_uint16
+        L.oracle_f16_to_f32.argtypes = [ctypes.c_uint16]
+        L.oracle_f16_to_f32.restype = ctypes.c_float
+        L.oracle_quantize_act.argtypes = [P, I64, I64, P, P]
+        L.oracle_quantize_act.restype = ctypes.c_int
+        L.oracle_linear_q.argtypes = [P, P, I64, I64, P, I64, P, P, ctypes.c_int, P, P, P, P, P]
+        L.oracle_linear_q.restype = ctypes.c_int
+        L.oracle_linear.argtypes = [P, I64, I64, P, I64, P, P, ctypes.c_int, P, P, P, P, P, P, P]
+        L.oracle_linear.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc, what):
+    if rc != OK:
+        raise ValueError(f"oracle {what} failed with code {rc}")
+
+
+def bf16_to_f32(bits: int) -> float:
+    return lib().oracle_bf16_to_f32(int(bits))
+
+
+def f32_to_bf16(v: float) -> int:
+    return lib().oracle_f32_to_bf16(float(v))
+
+
+def f16_to_f32(bits: int) -> float:
+    return lib().oracle_f16_to_f32(int(bits))
+
+
+def quantize_act(x_bits: np.ndarray):
+    """x_bits: uint16 bf16 patterns [M][K] -> (q int8 [M][K], s fp32 [M])."""
+    x = np.ascontiguousarray(x_bits, dtype=np.uint16)
+    M, K = x.shape
+    q = np.empty((M, K), np.int8)
+    s = np.empty((M,), np.float32)
+    _check(lib().oracle_quantize_act(_ptr(x), M, K, _ptr(q), _ptr(s)), "quantize_act")
+    return q, s
+
+
+def linear_q(q, s_x, w, s_w=None, s_g=None, nthreads=1):
+    """Linear layer on pre-quantized activations.  Returns a dict with
+    acc (int32), y32 (fp32), y (bf16 bits), y64 (fp64), bound (fp64)."""
+    q = np.ascontiguousarray(q, dtype=np.int8)
+    s_x = np.ascontiguousarray(s_x, dtype=np.float32)
+    w = np.ascontiguousarray(w, dtype=np.int8)
+    M, K = q.shape
+    N = w.shape[0]
+    assert w.shape == (N, K)
+    sw = None if s_w is None else np.ascontiguousarray(s_w, dtype=np.float32)
+    sg = None if s_g is None else np.ascontiguousarray(s_g).view(np.uint16)
+    out = dict(acc=np.empty((M, N), np.int32), y32=np.empty((M, N), np.float32),
+               y=np.empty((M, N), np.uint16), y64=np.empty((M, N), np.float64),
+               bound=np.empty((M, N), np.float64))
+    rc = lib().oracle_linear_q(_ptr(q), _ptr(s_x), M, K, _ptr(w), N, _ptr(sw), _ptr(sg),
+                               int(nthreads), _ptr(out["acc"]), _ptr(out["y32"]), _ptr(out["y"]),
+                               _ptr(out["y64"]), _ptr(out["bound"]))
+    _check(rc, "linear_q")
+    return out
+
+
+def linear(x_bits, w, s_w=None, s_g=None, nthreads=1):
+    """The whole path from bf16 activations.  Returns linear_q's dict plus
+    q (int8 [M][K]) and s_x (fp32 [M])."""
+    x = np.ascontiguousarray(x_bits, dtype=np.uint16)
+    w = np.ascontiguousarray(w, dtype=np.int8)
+    M, K = x.shape
+    N = w.shape[0]
+    assert w.shape == (N, K)
+    sw = None if s_w is None else np.ascontiguousarray(s_w, dtype=np.float32)
+    sg = None if s_g is None else np.ascontiguousarray(s_g).view(np.uint16)
+    out = dict(q=np.empty((M, K), np.int8), s_x=np.empty((M,), np.float32),
+               acc=np.empty((M, N), np.int32), y32=np.empty((M, N), np.float32),
+               y=np.empty((M, N), np.uint16), y64=np.empty((M, N), np.float64),
+               bound=np.empty((M, N), np.float64))
+    rc = lib().oracle_linear(_ptr(x), M, K, _ptr(w), N, _ptr(sw), _ptr(sg), int(nthreads),
+                             _ptr(out["q"]), _ptr(out["s_x"]), _ptr(out["acc"]), _ptr(out["y32"]),
+                             _ptr(out["y"]), _ptr(out["y64"]), _ptr(out["bound"]))
+    _check(rc, "linear")
+    return out

@@ -1,0 +1,336 @@
+"""Pins of the CPU oracle against facts fixed by the mathematics (no GPU).
+
+The paper prints no worked W4A8 example, so each oracle function is pinned
+by closed forms, special cases that reduce to a library routine (numpy's
+integer matmul, numpy's fp16 decode, torch's bf16 rounding), brute force on
+tiny inputs, and invariants chosen so that a dropped term, a wrong sign or
+index, or a transposed operand fails at least one test.
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_12932_amd import inputs as I
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rng(seed=0):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def bits_of(vals):
+    return I.to_bf16_bits(np.asarray(vals, np.float32))
+
+
+def f32_of_bits(b):
+    return (np.asarray(b, np.uint32) << 16).view(np.float32)
+
+
+# ---------------------------------------------------------------- formats
+
+def test_bf16_decode_exhaustive():
+    b = np.arange(65536, dtype=np.uint32)
+    want = (b << 16).view(np.float32)
+    L = oracle.lib()
+    sel = b[::7]
+    got = np.array([L.oracle_bf16_to_f32(int(v)) for v in sel], np.float32)
+    w = want[::7]
+    fin = ~np.isnan(w)   # a NaN may come back quieted through the C return path
+    np.testing.assert_array_equal(got[fin].view(np.uint32), w[fin].view(np.uint32))
+    assert np.all(np.isnan(got[~fin]))
+
+
+def test_bf16_rne_matches_torch_and_ties():
+    r = rng(1)
+    vals = r.standard_normal(20000).astype(np.float32) * np.float32(1e3)
+    vals = np.concatenate([vals, np.array([1.00390625, 1.01171875, -1.00390625, 0.0, -0.0,
+                                           3.0e38, 1e-40], np.float32)])
+    want = torch.from_numpy(vals).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = np.array([oracle.f32_to_bf16(float(v)) for v in vals], np.uint16)
+    np.testing.assert_array_equal(got, want)
+    # 1 + 2^-8 is a tie between 1.0 (even) and 1 + 2^-7: must go to 0x3F80.
+    assert oracle.f32_to_bf16(1.00390625) == 0x3F80
+    # 1 + 3*2^-8 is a tie between 1+2^-7 (odd) and 1+2^-6 (even): 0x3F82.
+    assert oracle.f32_to_bf16(1.01171875) == 0x3F82
+    assert oracle.f32_to_bf16(float("nan")) == 0x7FC0
+
+
+def test_f16_decode_exhaustive():
+    b = np.arange(65536, dtype=np.uint16)
+    want = b.view(np.float16).astype(np.float32)
+    got = np.array([oracle.f16_to_f32(int(v)) for v in b], np.float32)
+    fin = np.isfinite(want)
+    np.testing.assert_array_equal(got[fin].view(np.uint32), want[fin].view(np.uint32))
+    assert np.all(np.isnan(got[np.isnan(want)]))
+    assert np.all(got[np.isinf(want)] == want[np.isinf(want)])
+
+
+# ---------------------------------------------------------------- quantize
+
+def load_ties():
+    rows = []
+    with open(os.path.join(GOLDEN, "quant_ties.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            a, b = line.split()
+            rows.append((float(a), int(b)))
+    return rows
+
+
+def test_quantize_round_half_even_golden():
+    rows = load_ties()
+    x = bits_of([[v for v, _ in rows]])
+    q, s = oracle.quantize_act(x)
+    assert s[0] == np.float32(1.0)
+    assert q[0].tolist() == [e for _, e in rows]
+
+
+def test_quantize_zero_row_and_argmax():
+    x = I.activations(6, 512, 11)
+    x[2] = 0                                 # +0.0 row
+    x[4] = 0x8000                            # -0.0 row
+    q, s = oracle.quantize_act(x)
+    assert s[2] == 0 and s[4] == 0 and not q[2].any() and not q[4].any()
+    xf = f32_of_bits(x)
+    for m in (0, 1, 3, 5):
+        j = int(np.argmax(np.abs(xf[m])))
+        assert abs(int(q[m, j])) == 127
+        assert np.sign(q[m, j]) == np.sign(xf[m, j])
+        assert s[m] == np.float32(np.abs(xf[m]).max()) / np.float32(127.0)
+
+
+def test_quantize_properties():
+    x = I.activations(8, 1024, 12)
+    q, s = oracle.quantize_act(x)
+    xf = f32_of_bits(x).astype(np.float64)
+    assert np.abs(q).max() <= 127
+    # nearest-integer property of the code: |x/s - q| <= 1/2 (+ fp32 slack)
+    r = xf / s[:, None].astype(np.float64)
+    assert np.all(np.abs(r - q) <= 0.5 + 1e-5)
+    # negation symmetry
+    qn, sn = oracle.quantize_act(x ^ np.uint16(0x8000))
+    np.testing.assert_array_equal(sn, s)
+    np.testing.assert_array_equal(qn, -q)
+    # scaling a row by a power of two leaves the codes unchanged and scales s exactly
+    x4 = bits_of(f32_of_bits(x) * np.float32(4.0))
+    q4, s4 = oracle.quantize_act(x4)
+    np.testing.assert_array_equal(q4, q)
+    np.testing.assert_array_equal(s4, s * np.float32(4.0))
+
+
+def test_quantize_matches_numpy_ieee():
+    # numpy's fp32 division and rint implement the same IEEE operations as
+    # the oracle's C code, by an independent implementation.
+    x = I.activations(16, 4096, 13)
+    q, s = oracle.quantize_act(x)
+    xf = f32_of_bits(x)
+    a = np.abs(xf).max(axis=1)
+    s_np = (a / np.float32(127.0)).astype(np.float32)
+    q_np = np.clip(np.rint(xf / s_np[:, None]), -127, 127).astype(np.int8)
+    np.testing.assert_array_equal(s, s_np)
+    np.testing.assert_array_equal(q, q_np)
+
+
+def test_quantize_rejects_nonfinite():
+    x = I.activations(2, 256, 14)
+    x[1, 5] = 0x7F80  # +inf
+    with pytest.raises(ValueError):
+        oracle.quantize_act(x)
+
+
+# ---------------------------------------------------------------- contraction
+
+def brute_acc(q, w):
+    M, K = q.shape
+    N = w.shape[0]
+    return [[sum(int(q[m][k]) * int(w[n][k]) for k in range(K)) for n in range(N)] for m in range(M)]
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 1, 128), (3, 5, 128), (8, 8, 256), (2, 7, 384)])
+def test_acc_brute_force(M, N, K):
+    r = rng(M * 100 + N)
+    x = I.activations(M, K, 20 + M)
+    W = r.integers(-8, 8, size=(N, K), dtype=np.int8)
+    out = oracle.linear(x, W, s_w=np.ones(N, np.float32))
+    assert out["acc"].tolist() == brute_acc(out["q"], W)
+
+
+@pytest.mark.parametrize("M,N,K", [(4, 256, 256), (33, 96, 1024), (16, 64, 12288)])
+def test_acc_matches_numpy_matmul(M, N, K):
+    x = I.activations(M, K, 30 + M)
+    W, sw = I.weights(N, K, 40 + N)
+    out = oracle.linear(x, W, s_w=sw, nthreads=3)
+    ref = out["q"].astype(np.int64) @ W.astype(np.int64).T
+    np.testing.assert_array_equal(out["acc"].astype(np.int64), ref)
+
+
+def test_zero_weights_give_positive_zero():
+    x = I.activations(5, 256, 50)
+    W = np.zeros((64, 256), np.int8)
+    out = oracle.linear(x, W, s_w=np.full(64, 0.01, np.float32))
+    assert not out["acc"].any()
+    assert not out["y"].any()                     # +0.0 bf16 pattern
+    assert not out["y32"].view(np.uint32).any()
+    _, sg = I.weights(64, 256, 51, group=True)
+    outg = oracle.linear(x, W, s_g=sg)
+    assert not outg["y"].any() and not outg["y32"].view(np.uint32).any()
+
+
+@pytest.mark.parametrize("v", [1, 7, -8])
+def test_one_hot_row_selects_column(v):
+    K, N = 384, 16
+    x = I.activations(6, K, 60)
+    r = rng(61)
+    W = np.zeros((N, K), np.int8)
+    cols = r.integers(0, K, size=N)
+    W[np.arange(N), cols] = v
+    out = oracle.linear(x, W, s_w=np.ones(N, np.float32))
+    for n in range(N):
+        np.testing.assert_array_equal(out["acc"][:, n], v * out["q"][:, cols[n]].astype(np.int32))
+
+
+@pytest.mark.parametrize("K", [128, 4096, 12288])
+def test_closed_form_extremes(K):
+    x = np.stack([bits_of(np.ones(K)), bits_of(-np.ones(K))])
+    W = np.full((64, K), -8, np.int8)
+    out = oracle.linear(x, W, s_w=np.ones(64, np.float32))
+    assert (out["q"][0] == 127).all() and (out["q"][1] == -127).all()
+    assert (out["acc"][0] == -1016 * K).all()
+    assert (out["acc"][1] == 1016 * K).all()
+
+
+def test_additivity_in_weights():
+    K, N = 512, 32
+    x = I.activations(4, K, 70)
+    r = rng(71)
+    W1 = r.integers(-4, 4, size=(N, K), dtype=np.int8)
+    W2 = r.integers(-4, 4, size=(N, K), dtype=np.int8)
+    one = np.ones(N, np.float32)
+    a1 = oracle.linear(x, W1, s_w=one)["acc"].astype(np.int64)
+    a2 = oracle.linear(x, W2, s_w=one)["acc"].astype(np.int64)
+    a12 = oracle.linear(x, (W1 + W2).astype(np.int8), s_w=one)["acc"].astype(np.int64)
+    np.testing.assert_array_equal(a12, a1 + a2)
+
+
+def test_rejects_out_of_range_weights():
+    x = I.activations(1, 128, 72)
+    W = np.zeros((4, 128), np.int8)
+    W[2, 3] = 8
+    with pytest.raises(ValueError):
+        oracle.linear(x, W, s_w=np.ones(4, np.float32))
+
+
+# ---------------------------------------------------------------- dequant
+
+def test_per_channel_y64_exact_rational():
+    x = I.activations(3, 256, 80)
+    W, sw = I.weights(8, 256, 81)
+    out = oracle.linear(x, W, s_w=sw)
+    for m in range(3):
+        for n in range(8):
+            exact = Fraction(int(out["acc"][m, n])) * Fraction(float(out["s_x"][m])) * Fraction(float(sw[n]))
+            got = out["y64"][m, n]
+            assert abs(Fraction(got) - exact) <= abs(exact) * Fraction(1, 2**52)
+
+
+def test_bf16_output_is_rne_of_y32():
+    x = I.activations(8, 1024, 82)
+    W, sw = I.weights(128, 1024, 83)
+    out = oracle.linear(x, W, s_w=sw)
+    want = torch.from_numpy(out["y32"]).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(out["y"], want)
+    rel = np.abs(out["y32"].astype(np.float64) - out["y64"]) / np.maximum(np.abs(out["y64"]), 1e-30)
+    assert rel.max() < 2.0 ** -22
+
+
+def test_scale_linearity_power_of_two():
+    x = I.activations(8, 512, 84)
+    W, sw = I.weights(64, 512, 85)
+    a = oracle.linear(x, W, s_w=sw)
+    b = oracle.linear(x, W, s_w=sw * np.float32(2.0))
+    np.testing.assert_array_equal(b["y32"], a["y32"] * np.float32(2.0))
+    np.testing.assert_array_equal(b["y64"], a["y64"] * 2.0)
+    nz = a["y"] & 0x7FFF != 0
+    np.testing.assert_array_equal(b["y"][nz], a["y"][nz] + np.uint16(0x80))   # exponent + 1
+    # activation scale: doubling x doubles s_x and so y, codes unchanged
+    x2 = bits_of(f32_of_bits(x) * np.float32(2.0))
+    c = oracle.linear(x2, W, s_w=sw)
+    np.testing.assert_array_equal(c["q"], a["q"])
+    np.testing.assert_array_equal(c["y32"], a["y32"] * np.float32(2.0))
+
+
+def test_scale_linearity_general():
+    x = I.activations(4, 512, 86)
+    W, sw = I.weights(64, 512, 87)
+    a = oracle.linear(x, W, s_w=sw)
+    b = oracle.linear(x, W, s_w=(sw * np.float32(1.37)).astype(np.float32))
+    np.testing.assert_allclose(b["y64"], a["y64"] * 1.37, rtol=1e-6, atol=0)
+
+
+def test_group_k128_equals_per_channel():
+    x = I.activations(6, 128, 88)
+    W, sg = I.weights(64, 128, 89, group=True)
+    g = oracle.linear(x, W, s_g=sg)
+    c = oracle.linear(x, W, s_w=sg[0].astype(np.float32))
+    np.testing.assert_array_equal(g["acc"], c["acc"])
+    np.testing.assert_array_equal(g["y64"], c["y64"])
+
+
+def test_group_constant_along_k_equals_per_channel():
+    K, N = 1024, 64
+    x = I.activations(5, K, 90)
+    W, sw16 = I.weights(N, K, 91, group=True)
+    per_n = sw16[0]
+    sg = np.tile(per_n, (K // 128, 1))
+    g = oracle.linear(x, W, s_g=sg)
+    c = oracle.linear(x, W, s_w=per_n.astype(np.float32))
+    np.testing.assert_allclose(g["y64"], c["y64"], rtol=1e-12, atol=0)
+
+
+def test_group_indicator_selects_one_group():
+    # s_g = 1 on group g0 and 0 elsewhere reduces the group layer to a
+    # per-channel layer (unit scales) over the 128 columns of that group.
+    K, N = 768, 32
+    x = I.activations(4, K, 92)
+    W, _ = I.weights(N, K, 93)
+    full = oracle.linear(x, W, s_w=np.ones(N, np.float32))
+    for g0 in (0, 2, 5):
+        sg = np.zeros((K // 128, N), np.float16)
+        sg[g0] = 1.0
+        g = oracle.linear_q(full["q"], full["s_x"], W, s_g=sg)
+        sub = oracle.linear_q(full["q"][:, 128 * g0:128 * (g0 + 1)], np.ones(4, np.float32),
+                              W[:, 128 * g0:128 * (g0 + 1)], s_w=np.ones(N, np.float32))
+        np.testing.assert_array_equal(g["y64"], sub["acc"].astype(np.float64) * full["s_x"][:, None].astype(np.float64))
+    # and the group sum adds up: sum over indicators equals all-ones group scales
+    ones = oracle.linear_q(full["q"], full["s_x"], W, s_g=np.ones((K // 128, N), np.float16))
+    np.testing.assert_array_equal(ones["acc"], full["acc"])
+    np.testing.assert_allclose(ones["y64"], full["acc"] * full["s_x"][:, None].astype(np.float64), rtol=1e-15)
+
+
+def test_group_bound_dominates():
+    x = I.activations(4, 1024, 94)
+    W, sg = I.weights(64, 1024, 95, group=True)
+    g = oracle.linear(x, W, s_g=sg)
+    assert np.all(g["bound"] >= np.abs(g["y64"]) * (1 - 1e-12))
+    # a weight row of constant sign against a positive row makes all partials one-signed
+    xp = bits_of(np.abs(f32_of_bits(x)) + np.float32(0.5))
+    Wp = np.minimum(np.abs(W.astype(np.int16)), 7).astype(np.int8)
+    gp = oracle.linear(xp, Wp, s_g=sg)
+    np.testing.assert_allclose(gp["bound"], np.abs(gp["y64"]), rtol=1e-12)
+
+
+def test_threads_do_not_change_results():
+    x = I.activations(13, 512, 96)
+    W, sg = I.weights(64, 512, 97, group=True)
+    a = oracle.linear(x, W, s_g=sg, nthreads=1)
+    b = oracle.linear(x, W, s_g=sg, nthreads=5)
+    for k in ("acc", "y32", "y", "y64"):
+        np.testing.assert_array_equal(a[k], b[k])

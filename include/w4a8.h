@@ -1,0 +1,165 @@
+/*
+ * w4a8.h - C ABI of the MI355X (gfx950) W4A8 linear layer
+ *
+ *     y = dequant( quant8(x) . int4(W)^T )
+ *
+ * FlashDrive, Sec. 3.4 ("Quantization"): the backbone weights are held as
+ * 4-bit integers, the activations entering each backbone linear layer are
+ * cast to 8 bits, and the product runs on the integer matrix units; Sec. 4.2
+ * ("Algorithm-level gains", on Table 1) attributes the decode gain to the 4x
+ * smaller weight stream and the prefill gain to the INT8 contraction.  Sec.
+ * 3.5 ("Kernel Fusion") fuses Q/K/V into one projection and gate/up into
+ * another, which is why N can be 6144 or 24576 here.  The paper fixes no
+ * scale granularity or rounding; this library implements:
+ *   - per-token symmetric activation scale s_x[m] = max_k |x[m,k]| / 127 (fp32),
+ *     codes q[m,k] = round_half_even(x[m,k] / s_x[m]) in [-127, 127];
+ *     an all-zero token has s_x = 0 and q = 0;
+ *   - weight integers W[n,k] in [-8, 7] with either one fp32 scale per output
+ *     channel n, or one fp16 scale per 128 consecutive k per channel;
+ *   - an exact int32 contraction acc[m,n] = sum_k q[m,k] W[n,k];
+ *   - dequantization per channel: y = ((float)acc * s_x[m]) * s_w[n], two
+ *     fp32 multiplies in that order; per group: y = s_x[m] * sum_g
+ *     (float)p_g[m,n] * s_g[g][n] accumulated in fp32 (order unspecified);
+ *     bf16 outputs are rounded to nearest even.
+ *
+ * Conventions for every call:
+ *   - Matrices are dense and row-major (last index contiguous): x [M][K],
+ *     W [N][K] (the nn.Linear weight layout, so y = x W^T), y [M][N].
+ *   - Pointers named "device" are HIP device pointers; the caller allocates
+ *     and owns every buffer; the library never allocates device memory on
+ *     these calls and keeps no pointer after a call returns.
+ *   - Work is enqueued on `stream` (0 = the null stream) and is asynchronous
+ *     unless the call says otherwise; calls on different streams do not share
+ *     state, except that concurrent w4a8_linear calls must not share one
+ *     workspace.
+ *   - Arguments are validated before anything is launched; an invalid call
+ *     returns an error code and has no effect.  No call prints or aborts.
+ *   - A HIP launch failure is reported as W4A8_EHIP.
+ */
+#ifndef W4A8_H_
+#define W4A8_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  W4A8_OK = 0,
+  W4A8_EINVAL = 1,       /* null/misaligned pointer, bad size, mode, or workspace too small */
+  W4A8_EUNSUPPORTED = 2, /* well-formed but outside the supported shape range */
+  W4A8_ERANGE = 3,       /* a weight value outside [-8, 7] */
+  W4A8_EHIP = 4          /* the HIP runtime reported an error */
+} w4a8_status;
+
+/* weight scale granularity */
+typedef enum {
+  W4A8_SCALE_CHANNEL_F32 = 0, /* w_scale: fp32 [N] */
+  W4A8_SCALE_GROUP_F16 = 1    /* w_scale: fp16 [K/128][N], group of 128 along k */
+} w4a8_scale_mode;
+
+/* activation input of w4a8_linear */
+typedef enum {
+  W4A8_IN_BF16 = 0, /* x: bf16 [M][K]; quantized inside the call */
+  W4A8_IN_I8 = 1    /* x: int8 codes [M][K] with x_scale fp32 [M] (w4a8_quantize_act output) */
+} w4a8_in_kind;
+
+/* output of w4a8_linear */
+typedef enum {
+  W4A8_OUT_BF16 = 0,   /* y: bf16 [M][N] */
+  W4A8_OUT_F32 = 1,    /* y: fp32 [M][N], the value before bf16 rounding */
+  W4A8_OUT_I32_ACC = 2 /* y: int32 [M][N], the raw accumulator sum_k q W (scales unused) */
+} w4a8_out_kind;
+
+#define W4A8_GROUP_SIZE 128
+#define W4A8_K_MAX 65536     /* 16 * 127 * 8 * K stays below 2^31 */
+#define W4A8_M_MAX 1048576
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* w4a8_status_string(w4a8_status s);
+
+/*
+ * Size in bytes of the packed weight buffer for an N x K weight: N*K/2
+ * (two 4-bit values per byte, the 4x reduction of Sec. 3.4's memory saving
+ * against 16-bit weights).  Returns 0 if N or K is not a valid shape
+ * (N % 16 != 0, K % 128 != 0, or out of range).
+ */
+size_t w4a8_packed_weight_bytes(int64_t N, int64_t K);
+
+/*
+ * Pack int4-range weights for w4a8_linear (one-time, off the hot path).
+ *   w         device, int8 [N][K], every value in [-8, 7]
+ *   N, K      N % 16 == 0, K % 128 == 0, 1 <= K <= W4A8_K_MAX
+ *   w_packed  device, w4a8_packed_weight_bytes(N, K) bytes, 16-byte aligned;
+ *             the layout is opaque (ordered for the matrix-core operand
+ *             fragments) and only w4a8_linear reads it
+ * Synchronizes `stream`.  Returns W4A8_ERANGE (w_packed then holds garbage)
+ * if any value lies outside [-8, 7].  Calls from several host threads are
+ * serialized internally.
+ */
+w4a8_status w4a8_pack_weights(const int8_t* w, int64_t N, int64_t K, uint8_t* w_packed,
+                              hipStream_t stream);
+
+/*
+ * Per-token symmetric int8 quantization (the 8-bit activation cast of
+ * Sec. 3.4), exactly as defined at the top of this header.
+ *   x        device, bf16 bit patterns [M][K], finite values, 16-byte aligned
+ *   M, K     0 <= M <= W4A8_M_MAX, K % 128 == 0, K <= W4A8_K_MAX; M == 0 is a no-op
+ *   x_q      device, int8 [M][K], 16-byte aligned
+ *   x_scale  device, fp32 [M], 4-byte aligned
+ * Results are bit-identical to the IEEE-754 fp32 definition (division and
+ * round-half-even).  Non-finite inputs give unspecified codes.
+ */
+w4a8_status w4a8_quantize_act(const uint16_t* x, int64_t M, int64_t K, int8_t* x_q,
+                              float* x_scale, hipStream_t stream);
+
+/*
+ * Bytes of device workspace w4a8_linear needs for this problem (0 if none).
+ * The workspace holds split-K partial sums and arrival counters (and, for
+ * large M with bf16 input, the int8 codes and scales).  The caller must
+ * zero-fill a workspace once before its first use; every call leaves its
+ * counters at zero again, so the same workspace can be reused by later
+ * calls on the same stream.  Returns 0 as well for invalid shapes.
+ */
+size_t w4a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind);
+
+/*
+ * The W4A8 linear layer: y[M][N] = dequant(quant8(x) . W^T).
+ *   x              device, bf16 [M][K] (in_kind W4A8_IN_BF16) or int8 codes
+ *                  [M][K] (W4A8_IN_I8), 16-byte aligned
+ *   x_scale        device, fp32 [M] (W4A8_IN_I8 only, else ignored)
+ *   M, K           0 <= M <= W4A8_M_MAX (M == 0 is a no-op), K % 128 == 0,
+ *                  128 <= K <= W4A8_K_MAX
+ *   w_packed       device, from w4a8_pack_weights with the same N, K
+ *   w_scale        device, fp32 [N] or fp16 [K/128][N] per scale_mode; unused
+ *                  for W4A8_OUT_I32_ACC
+ *   N              N % 16 == 0
+ *   y              device, [M][N] of out_kind, 16-byte aligned
+ *   workspace      device, >= w4a8_linear_workspace_bytes(...) bytes, 256-byte
+ *                  aligned, zero-filled before its first use (may be NULL if
+ *                  the size is 0)
+ * Does not synchronize.  Deterministic: the same inputs give the same bits.
+ */
+w4a8_status w4a8_linear(const void* x, int in_kind, const float* x_scale, int64_t M, int64_t K,
+                        const uint8_t* w_packed, const void* w_scale, int scale_mode, int64_t N,
+                        void* y, int out_kind, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+
+/*
+ * Introspection for benchmarks and tests: a static, thread-local text
+ * naming the kernels and tiling w4a8_linear would use for this problem and
+ * its workspace size ("invalid shape" for a shape w4a8_linear rejects).
+ * Enqueues nothing.
+ */
+const char* w4a8_linear_describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind,
+                                 int out_kind);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* W4A8_H_ */

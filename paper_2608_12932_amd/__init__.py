@@ -1,0 +1,189 @@
+"""MI355X (gfx950) W4A8 linear layer: Python binding of libw4a8.so.
+
+The functions carry the names of the C ABI in include/w4a8.h and only
+marshal arguments: they check dtypes and shapes of torch tensors, allocate
+outputs with torch (device memory is the one thing torch is used for here),
+and pass raw pointers plus torch's current HIP stream to the library.  Every
+step of the computation runs in the HIP kernels; there is no fallback, and
+loading fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libw4a8.so")
+
+W4A8_OK, W4A8_EINVAL, W4A8_EUNSUPPORTED, W4A8_ERANGE, W4A8_EHIP = 0, 1, 2, 3, 4
+SCALE_CHANNEL_F32, SCALE_GROUP_F16 = 0, 1
+IN_BF16, IN_I8 = 0, 1
+OUT_BF16, OUT_F32, OUT_I32_ACC = 0, 1, 2
+GROUP_SIZE = 128
+
+EXPORTS = ("w4a8_status_string", "w4a8_packed_weight_bytes", "w4a8_pack_weights",
+           "w4a8_quantize_act", "w4a8_linear_workspace_bytes", "w4a8_linear",
+           "w4a8_linear_describe")
+
+_OUT_DTYPE = {OUT_BF16: torch.bfloat16, OUT_F32: torch.float32, OUT_I32_ACC: torch.int32}
+
+
+class W4A8Error(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libw4a8.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(hipcc, gfx950) before using the W4A8 kernels")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I64, I, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+        L.w4a8_status_string.argtypes = [I]
+        L.w4a8_status_string.restype = ctypes.c_char_p
+        L.w4a8_packed_weight_bytes.argtypes = [I64, I64]
+        L.w4a8_packed_weight_bytes.restype = SZ
+        L.w4a8_pack_weights.argtypes = [P, I64, I64, P, P]
+        L.w4a8_pack_weights.restype = I
+        L.w4a8_quantize_act.argtypes = [P, I64, I64, P, P, P]
+        L.w4a8_quantize_act.restype = I
+        L.w4a8_linear_workspace_bytes.argtypes = [I64, I64, I64, I, I]
+        L.w4a8_linear_workspace_bytes.restype = SZ
+        L.w4a8_linear.argtypes = [P, I, P, I64, I64, P, P, I, I64, P, I, P, SZ, P]
+        L.w4a8_linear.restype = I
+        L.w4a8_linear_describe.argtypes = [I64, I64, I64, I, I, I]
+        L.w4a8_linear_describe.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().w4a8_status_string(int(status)).decode()
+
+
+def _stream(stream=None) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _dev(t: torch.Tensor, name: str, dtype: torch.dtype) -> int:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _check(rc: int, what: str) -> None:
+    if rc != W4A8_OK:
+        raise W4A8Error(rc, what)
+
+
+def w4a8_packed_weight_bytes(N: int, K: int) -> int:
+    return int(lib().w4a8_packed_weight_bytes(N, K))
+
+
+def w4a8_pack_weights(w: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """w: int8 [N][K] device tensor with values in [-8, 7] -> packed uint8 (N*K/2)."""
+    N, K = w.shape
+    nbytes = w4a8_packed_weight_bytes(N, K)
+    if nbytes == 0:
+        raise W4A8Error(W4A8_EINVAL, f"w4a8_pack_weights: shape {N}x{K}")
+    if out is None:
+        out = torch.empty(nbytes, dtype=torch.uint8, device=w.device)
+    elif out.numel() != nbytes:
+        raise ValueError(f"out must hold {nbytes} bytes")
+    rc = lib().w4a8_pack_weights(_dev(w, "w", torch.int8), N, K, _dev(out, "out", torch.uint8),
+                                 _stream(stream))
+    _check(rc, "w4a8_pack_weights")
+    return out
+
+
+def w4a8_quantize_act(x: torch.Tensor, stream=None):
+    """x: bf16 [M][K] device tensor -> (codes int8 [M][K], scales fp32 [M])."""
+    M, K = x.shape
+    q = torch.empty((M, K), dtype=torch.int8, device=x.device)
+    s = torch.empty((M,), dtype=torch.float32, device=x.device)
+    rc = lib().w4a8_quantize_act(_dev(x, "x", torch.bfloat16), M, K, _dev(q, "q", torch.int8),
+                                 _dev(s, "s", torch.float32), _stream(stream))
+    _check(rc, "w4a8_quantize_act")
+    return q, s
+
+
+def w4a8_linear_workspace_bytes(M: int, N: int, K: int, scale_mode: int = SCALE_CHANNEL_F32,
+                                in_kind: int = IN_BF16) -> int:
+    return int(lib().w4a8_linear_workspace_bytes(M, N, K, scale_mode, in_kind))
+
+
+def w4a8_linear_describe(M: int, N: int, K: int, scale_mode: int = SCALE_CHANNEL_F32,
+                         in_kind: int = IN_BF16, out_kind: int = OUT_BF16) -> str:
+    return lib().w4a8_linear_describe(M, N, K, scale_mode, in_kind, out_kind).decode()
+
+
+class Workspace:
+    """A zero-filled device buffer reused across w4a8_linear calls on one
+    stream (the calls leave its counters at zero).  Grows on demand."""
+
+    def __init__(self, device="cuda"):
+        self.device = torch.device(device)
+        self.buf = torch.zeros(0, dtype=torch.uint8, device=self.device)
+
+    def get(self, nbytes: int) -> torch.Tensor:
+        if nbytes > self.buf.numel():
+            self.buf = torch.zeros(max(nbytes, 2 * self.buf.numel()), dtype=torch.uint8, device=self.device)
+        return self.buf
+
+
+def w4a8_linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor | None, N: int, *,
+                x_scale: torch.Tensor | None = None, scale_mode: int = SCALE_CHANNEL_F32,
+                out_kind: int = OUT_BF16, out: torch.Tensor | None = None,
+                workspace: Workspace | torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """y[M][N] = dequant(quant8(x) . W^T).
+
+    x is bf16 [M][K] (quantized inside the call) or int8 codes [M][K] with
+    x_scale fp32 [M].  w_scale is fp32 [N] (SCALE_CHANNEL_F32) or fp16
+    [K/128][N] (SCALE_GROUP_F16).  Returns bf16, fp32 or int32 [M][N].
+    """
+    M, K = x.shape
+    if x.dtype == torch.bfloat16:
+        in_kind = IN_BF16
+        xs_ptr = None
+    elif x.dtype == torch.int8:
+        in_kind = IN_I8
+        if x_scale is None:
+            raise ValueError("int8 input needs x_scale")
+        xs_ptr = _dev(x_scale, "x_scale", torch.float32)
+    else:
+        raise TypeError("x must be bf16 or int8")
+    x_ptr = _dev(x, "x", x.dtype)
+    wp_ptr = _dev(w_packed, "w_packed", torch.uint8)
+    if w_scale is None:
+        ws_ptr = None
+    else:
+        ws_ptr = _dev(w_scale, "w_scale", torch.float32 if scale_mode == SCALE_CHANNEL_F32 else torch.float16)
+    if out is None:
+        out = torch.empty((M, N), dtype=_OUT_DTYPE[out_kind], device=x.device)
+    y_ptr = _dev(out, "out", _OUT_DTYPE[out_kind])
+    need = w4a8_linear_workspace_bytes(M, N, K, scale_mode, in_kind)
+    if need == 0:
+        wk_ptr, wk_bytes = None, 0
+    else:
+        if workspace is None:
+            workspace = torch.zeros(need, dtype=torch.uint8, device=x.device)
+        buf = workspace.get(need) if isinstance(workspace, Workspace) else workspace
+        wk_ptr, wk_bytes = _dev(buf, "workspace", torch.uint8), buf.numel()
+    rc = lib().w4a8_linear(x_ptr, in_kind, xs_ptr, M, K, wp_ptr, ws_ptr, scale_mode, N, y_ptr,
+                           out_kind, wk_ptr, wk_bytes, _stream(stream))
+    _check(rc, "w4a8_linear")
+    return out

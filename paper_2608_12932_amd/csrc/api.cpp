@@ -1,0 +1,213 @@
+// C ABI of the W4A8 linear layer (declared in include/w4a8.h): argument
+// validation, the choice of kernel path and tiling, workspace layout and
+// launches.  Every check runs before anything is enqueued, so a rejected
+// call has no effect and touches no HIP state.
+#include "w4a8.h"
+
+#include <cstdio>
+#include <mutex>
+
+#include "kernels.h"
+
+using namespace w4a8;
+
+namespace {
+
+constexpr int64_t kNMax = int64_t(1) << 24;
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool valid_nk(int64_t N, int64_t K) {
+  return N >= 16 && N % 16 == 0 && N <= kNMax && K >= W4A8_GROUP_SIZE && K % W4A8_GROUP_SIZE == 0 &&
+         K <= W4A8_K_MAX;
+}
+
+// Everything w4a8_linear decides from the shapes and modes alone.
+struct Plan {
+  bool small_m = false;
+  bool separate_quant = false;  // bf16 input quantized by its own kernel first
+  SmallMPlan sm{};
+  LargeMPlan lm{};
+  // workspace layout (bytes)
+  size_t off_counters = 0, off_partial = 0, off_xq = 0, off_sx = 0, total = 0;
+};
+
+Plan make_plan(int64_t M, int64_t N, int64_t K, bool group, bool bf16_in) {
+  Plan p;
+  p.small_m = M <= kSmallMMaxM;
+  size_t off = 0;
+  if (p.small_m) {
+    p.sm = plan_smallm((int)M, (int)N, (int)K, group, bf16_in);
+    p.separate_quant = bf16_in && !p.sm.fused;
+    if (p.sm.S > 1) {
+      p.off_counters = off;
+      off = round_up(off + (size_t)p.sm.groups * sizeof(unsigned), 256);
+      p.off_partial = off;
+      off = round_up(off + (size_t)p.sm.S * M * N * 4, 256);
+    }
+  } else {
+    p.lm = plan_largem((int)M, (int)N, (int)K, group);
+    p.separate_quant = bf16_in;
+  }
+  if (p.separate_quant) {
+    p.off_xq = off;
+    off = round_up(off + (size_t)M * K, 256);
+    p.off_sx = off;
+    off = round_up(off + (size_t)M * sizeof(float), 256);
+  }
+  p.total = off;
+  return p;
+}
+
+std::mutex g_pack_mutex;
+
+}  // namespace
+
+extern "C" {
+
+const char* w4a8_status_string(w4a8_status s) {
+  switch (s) {
+    case W4A8_OK: return "ok";
+    case W4A8_EINVAL: return "invalid argument";
+    case W4A8_EUNSUPPORTED: return "unsupported shape";
+    case W4A8_ERANGE: return "weight value outside [-8, 7]";
+    case W4A8_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+size_t w4a8_packed_weight_bytes(int64_t N, int64_t K) {
+  if (!valid_nk(N, K)) return 0;
+  return (size_t)N * (size_t)K / 2;
+}
+
+w4a8_status w4a8_pack_weights(const int8_t* w, int64_t N, int64_t K, uint8_t* w_packed,
+                              hipStream_t stream) {
+  if (!valid_nk(N, K)) return W4A8_EINVAL;
+  if (!w || !w_packed || !aligned(w, 16) || !aligned(w_packed, 16)) return W4A8_EINVAL;
+  std::lock_guard<std::mutex> lk(g_pack_mutex);
+  unsigned* err = nullptr;
+  if (pack_error_word(&err) != hipSuccess) return W4A8_EHIP;
+  if (launch_pack(w, (int)N, (int)K, w_packed, err, stream) != hipSuccess) return W4A8_EHIP;
+  unsigned flag = 0;
+  if (hipMemcpyAsync(&flag, err, sizeof flag, hipMemcpyDeviceToHost, stream) != hipSuccess) return W4A8_EHIP;
+  if (hipStreamSynchronize(stream) != hipSuccess) return W4A8_EHIP;
+  return flag ? W4A8_ERANGE : W4A8_OK;
+}
+
+w4a8_status w4a8_quantize_act(const uint16_t* x, int64_t M, int64_t K, int8_t* x_q, float* x_scale,
+                              hipStream_t stream) {
+  if (M < 0 || M > W4A8_M_MAX) return W4A8_EINVAL;
+  if (K < W4A8_GROUP_SIZE || K % W4A8_GROUP_SIZE || K > W4A8_K_MAX) return W4A8_EINVAL;
+  if (M == 0) return W4A8_OK;
+  if (!x || !x_q || !x_scale || !aligned(x, 16) || !aligned(x_q, 16) || !aligned(x_scale, 4))
+    return W4A8_EINVAL;
+  return launch_quantize(x, (int)M, (int)K, x_q, x_scale, stream) == hipSuccess ? W4A8_OK : W4A8_EHIP;
+}
+
+size_t w4a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind) {
+  if (M < 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return 0;
+  if (scale_mode != W4A8_SCALE_CHANNEL_F32 && scale_mode != W4A8_SCALE_GROUP_F16) return 0;
+  if (in_kind != W4A8_IN_BF16 && in_kind != W4A8_IN_I8) return 0;
+  if (M == 0) return 0;
+  return make_plan(M, N, K, scale_mode == W4A8_SCALE_GROUP_F16, in_kind == W4A8_IN_BF16).total;
+}
+
+const char* w4a8_linear_describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind,
+                                 int out_kind) {
+  static thread_local char buf[256];
+  if (M <= 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return "invalid shape";
+  const bool group = scale_mode == W4A8_SCALE_GROUP_F16 && out_kind != W4A8_OUT_I32_ACC;
+  const Plan p = make_plan(M, N, K, group, in_kind == W4A8_IN_BF16);
+  if (p.small_m) {
+    SmallMPlan sm = p.sm;
+    sm.group = group;
+    snprintf(buf, sizeof buf, "%s%s workspace=%zu", p.separate_quant ? "quantize_rows + " : "",
+             smallm_kernel_name(sm), p.total);
+  } else {
+    snprintf(buf, sizeof buf, "%s%s workspace=%zu", p.separate_quant ? "quantize_rows + " : "",
+             largem_kernel_name(p.lm), p.total);
+  }
+  return buf;
+}
+
+w4a8_status w4a8_linear(const void* x, int in_kind, const float* x_scale, int64_t M, int64_t K,
+                        const uint8_t* w_packed, const void* w_scale, int scale_mode, int64_t N,
+                        void* y, int out_kind, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream) {
+  if (M < 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return W4A8_EINVAL;
+  if (in_kind != W4A8_IN_BF16 && in_kind != W4A8_IN_I8) return W4A8_EINVAL;
+  if (scale_mode != W4A8_SCALE_CHANNEL_F32 && scale_mode != W4A8_SCALE_GROUP_F16) return W4A8_EINVAL;
+  if (out_kind != W4A8_OUT_BF16 && out_kind != W4A8_OUT_F32 && out_kind != W4A8_OUT_I32_ACC)
+    return W4A8_EINVAL;
+  if (M == 0) return W4A8_OK;
+  if (!x || !aligned(x, 16) || !w_packed || !aligned(w_packed, 16) || !y || !aligned(y, 16))
+    return W4A8_EINVAL;
+  if (in_kind == W4A8_IN_I8 && (!x_scale || !aligned(x_scale, 4))) return W4A8_EINVAL;
+  if (out_kind != W4A8_OUT_I32_ACC &&
+      (!w_scale || !aligned(w_scale, scale_mode == W4A8_SCALE_CHANNEL_F32 ? 4 : 2)))
+    return W4A8_EINVAL;
+
+  // The integer accumulator does not depend on the scales, so the raw
+  // accumulator output always takes the per-channel kernels.
+  const bool group = scale_mode == W4A8_SCALE_GROUP_F16 && out_kind != W4A8_OUT_I32_ACC;
+  const bool bf16_in = in_kind == W4A8_IN_BF16;
+  const Plan p = make_plan(M, N, K, group, bf16_in);
+  if (workspace_bytes < p.total) return W4A8_EINVAL;
+  if (p.total && (!workspace || !aligned(workspace, 256))) return W4A8_EINVAL;
+
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  const void* xin = x;
+  const float* sx = x_scale;
+  if (p.separate_quant) {
+    int8_t* xq = reinterpret_cast<int8_t*>(ws + p.off_xq);
+    float* s = reinterpret_cast<float*>(ws + p.off_sx);
+    if (launch_quantize(static_cast<const uint16_t*>(x), (int)M, (int)K, xq, s, stream) != hipSuccess)
+      return W4A8_EHIP;
+    xin = xq;
+    sx = s;
+  }
+
+  hipError_t e;
+  if (p.small_m) {
+    SmallMPlan sm = p.sm;
+    sm.group = group;
+    if (!sm.fused || !bf16_in) sm.fused = false;
+    SmallMArgs a{};
+    a.x = xin;
+    a.x_scale = sx;
+    a.wp = w_packed;
+    a.w_scale = w_scale;
+    a.y = y;
+    a.partial = sm.S > 1 ? ws + p.off_partial : nullptr;
+    a.counters = sm.S > 1 ? reinterpret_cast<unsigned*>(ws + p.off_counters) : nullptr;
+    a.M = (int)M;
+    a.N = (int)N;
+    a.K = (int)K;
+    a.KB = (int)(K / W4A8_GROUP_SIZE);
+    a.S = sm.S;
+    a.kbs = (a.KB + sm.S - 1) / sm.S;
+    a.out_kind = out_kind;
+    e = launch_smallm(sm, a, stream);
+  } else {
+    LargeMArgs a{};
+    a.xq = static_cast<const int8_t*>(xin);
+    a.x_scale = sx;
+    a.wp = w_packed;
+    a.w_scale = w_scale;
+    a.y = y;
+    a.M = (int)M;
+    a.N = (int)N;
+    a.K = (int)K;
+    a.KB = (int)(K / W4A8_GROUP_SIZE);
+    a.out_kind = out_kind;
+    a.tiles_m = p.lm.tiles_m;
+    a.tiles_n = p.lm.tiles_n;
+    a.xcd_remap = (p.lm.tiles_m * p.lm.tiles_n) % 8 == 0;
+    e = launch_largem(p.lm, a, stream);
+  }
+  return e == hipSuccess ? W4A8_OK : W4A8_EHIP;
+}
+
+}  // extern "C"

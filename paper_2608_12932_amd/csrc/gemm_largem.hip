@@ -1,0 +1,268 @@
+// Large-M W4A8 GEMM (streaming prefill of new-frame tokens, M > 64).
+//
+// At large M the layer is bound by the INT8 contraction (FlashDrive
+// Sec. 4.2: prefill gains from the INT8 matrix units), so the kernel keeps
+// the matrix cores fed:
+//   - a BM x BN output tile per workgroup, 128 k per step (one scale group);
+//     tile sizes are picked on the host so that the tile count fills the 256
+//     CUs in whole waves;
+//   - each step's int8 activation tile and packed int4 weight tile are
+//     loaded into registers one step ahead and written into the other half
+//     of a double-buffered LDS stage (one barrier per step);
+//   - activation rows are XOR-swizzled in LDS (16-byte chunk c of row r at
+//     c ^ (r & 7)) so the 32 row reads of an MFMA operand hit distinct banks;
+//     weight chunks keep the packed order, which is already conflict free;
+//   - every wave holds a (32 WM) x (32 WN) accumulator tile of
+//     v_mfma_i32_32x32x32_i8 blocks; the weight nibbles are unpacked in
+//     registers right before the MFMAs;
+//   - workgroups are renumbered so that the tiles given to one XCD (the
+//     hardware deals workgroups to the 8 XCDs round robin) share their
+//     activation rows in that XCD's L2.
+// The epilogue applies per-token and per-channel scales (or, in group mode,
+// each step's int32 partial is rescaled by its fp16 group scale into an
+// fp32 accumulator).
+#include <cstdio>
+
+#include "device.h"
+#include "kernels.h"
+
+namespace w4a8 {
+
+namespace {
+
+template <int WM, int WN, int GM, int GN, bool GROUP>
+__global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
+  constexpr int kThreads = GM * GN * 64;
+  constexpr int BM = 32 * WM * GM, BN = 32 * WN * GN;
+  constexpr int kABytes = BM * 128, kBBytes = BN / 16 * kBlockBytes;
+  constexpr int kStage = kABytes + kBBytes;
+  constexpr int kACh = kABytes / 16 / kThreads, kBCh = kBBytes / 16 / kThreads;
+  static_assert(kACh * kThreads * 16 == kABytes, "A tile must split evenly over the threads");
+  static_assert(kBCh * kThreads * 16 == kBBytes, "B tile must split evenly over the threads");
+  extern __shared__ __align__(16) uint8_t lds[];
+
+  int bid = blockIdx.x;
+  const int total = a.tiles_m * a.tiles_n;
+  if (a.xcd_remap) bid = (bid & 7) * (total >> 3) + (bid >> 3);
+  const int tm = bid % a.tiles_m, tn = bid / a.tiles_m;
+  const int m0 = tm * BM, n0 = tn * BN, nt0 = n0 / 16;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % GM, wn = wave / GM;
+  const int M = a.M, N = a.N, K = a.K, KB = a.KB;
+  const int ntiles = N / 16;
+  const int l32 = lane & 31, g2 = lane >> 5;
+
+  uint4 ra[kACh], rb[kBCh];
+  auto gload = [&](int kb) {
+#pragma unroll
+    for (int i = 0; i < kACh; ++i) {
+      const int idx = tid + i * kThreads;
+      const int row = idx >> 3, ch = idx & 7;
+      const int grow = m0 + row;
+      ra[i] = grow < M ? *reinterpret_cast<const uint4*>(a.xq + (size_t)grow * K + kb * 128 + ch * 16)
+                       : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < kBCh; ++i) {
+      const int idx = tid + i * kThreads;
+      const int blk = idx >> 6, j = idx & 63;
+      const int tile = nt0 + blk;
+      rb[i] = tile < ntiles
+                  ? ldg_nt(reinterpret_cast<const uint4*>(a.wp + ((size_t)tile * KB + kb) * kBlockBytes) + j)
+                  : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto swrite = [&](int buf) {
+    uint8_t* As = lds + buf * kStage;
+    uint8_t* Bs = As + kABytes;
+#pragma unroll
+    for (int i = 0; i < kACh; ++i) {
+      const int idx = tid + i * kThreads;
+      const int row = idx >> 3, ch = idx & 7;
+      *reinterpret_cast<uint4*>(As + row * 128 + ((ch ^ (row & 7)) << 4)) = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < kBCh; ++i) {
+      const int idx = tid + i * kThreads;
+      *reinterpret_cast<uint4*>(Bs + idx * 16) = rb[i];
+    }
+  };
+
+  v16i acc[WM][WN];
+  float facc[GROUP ? WM : 1][GROUP ? WN : 1][16];
+#pragma unroll
+  for (int i = 0; i < WM; ++i)
+#pragma unroll
+    for (int j = 0; j < WN; ++j) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
+      if constexpr (GROUP)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) facc[i][j][r] = 0.0f;
+    }
+
+  gload(0);
+  swrite(0);
+  __syncthreads();
+  for (int kb = 0; kb < KB; ++kb) {
+    const int buf = kb & 1;
+    if (kb + 1 < KB) gload(kb + 1);
+    float sg[GROUP ? WN : 1];
+    if constexpr (GROUP) {
+      const uint16_t* sgp = static_cast<const uint16_t*>(a.w_scale);
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        const int col = n0 + wn * 32 * WN + j * 32 + l32;
+        sg[j] = col < N ? f16_to_f32(sgp[(size_t)kb * N + col]) * 0.0625f : 0.0f;
+      }
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
+    }
+    const uint8_t* As = lds + buf * kStage;
+    const uint8_t* Bs = As + kABytes;
+#pragma unroll
+    for (int tp = 0; tp < 2; ++tp) {
+      const int g = tp * 2 + g2;
+      v4i alo[WM], ahi[WM], blo[WN], bhi[WN];
+#pragma unroll
+      for (int i = 0; i < WM; ++i) {
+        const int row = wm * 32 * WM + i * 32 + l32;
+        const uint8_t* rp = As + row * 128;
+        alo[i] = *reinterpret_cast<const v4i*>(rp + (((2 * g) ^ (row & 7)) << 4));
+        ahi[i] = *reinterpret_cast<const v4i*>(rp + (((2 * g + 1) ^ (row & 7)) << 4));
+      }
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        const int col = wn * 32 * WN + j * 32 + l32;
+        const uint4 w = *reinterpret_cast<const uint4*>(Bs + (col >> 4) * kBlockBytes + (g * 16 + (col & 15)) * 16);
+        blo[j] = nib_lo(w);
+        bhi[j] = nib_hi(w);
+      }
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+          acc[i][j] = mfma32(alo[i], blo[j], acc[i][j]);
+          acc[i][j] = mfma32(ahi[i], bhi[j], acc[i][j]);
+        }
+    }
+    if constexpr (GROUP) {
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) facc[i][j][r] = __fmaf_rn((float)acc[i][j][r], sg[j], facc[i][j][r]);
+    }
+    if (kb + 1 < KB) swrite(buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: lane holds column l32, rows 8 (r / 4) + 4 g2 + r % 4
+#pragma unroll
+  for (int i = 0; i < WM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m0 + wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3);
+      if (row >= M) continue;
+      const float sx = a.out_kind == kOutI32 ? 0.0f : a.x_scale[row];
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        const int col = n0 + wn * 32 * WN + j * 32 + l32;
+        if (col >= N) continue;
+        const size_t o = (size_t)row * N + col;
+        float y32;
+        if constexpr (GROUP) {
+          y32 = __fmul_rn(facc[i][j][r], sx);
+        } else {
+          const int v = acc[i][j][r] >> 4;
+          if (a.out_kind == kOutI32) {
+            static_cast<int*>(a.y)[o] = v;
+            continue;
+          }
+          y32 = __fmul_rn(__fmul_rn((float)v, sx), static_cast<const float*>(a.w_scale)[col]);
+        }
+        if (a.out_kind == kOutF32)
+          static_cast<float*>(a.y)[o] = y32;
+        else
+          static_cast<uint16_t*>(a.y)[o] = (uint16_t)f32_to_bf16(y32);
+      }
+    }
+  }
+}
+
+typedef void (*LargeMKernel)(const LargeMArgs);
+
+struct TileCfg {
+  int WM, WN, GM, GN;
+  double quality;  // relative efficiency of the tile shape (operand reuse)
+};
+// BM = 32 WM GM, BN = 32 WN GN
+constexpr TileCfg kMenu[] = {
+    {2, 3, 2, 2, 1.00},  // 128 x 192, 4 waves
+    {2, 2, 2, 2, 0.95},  // 128 x 128, 4 waves
+    {1, 3, 2, 1, 0.85},  // 64 x 96, 2 waves
+    {1, 1, 2, 2, 0.70},  // 64 x 64, 4 waves
+};
+constexpr int kMenuSize = sizeof(kMenu) / sizeof(kMenu[0]);
+
+template <bool GROUP>
+LargeMKernel pick_cfg(int cfg) {
+  switch (cfg) {
+    case 0: return largem<2, 3, 2, 2, GROUP>;
+    case 1: return largem<2, 2, 2, 2, GROUP>;
+    case 2: return largem<1, 3, 2, 1, GROUP>;
+    case 3: return largem<1, 1, 2, 2, GROUP>;
+    default: return nullptr;
+  }
+}
+
+}  // namespace
+
+LargeMPlan plan_largem(int M, int N, int K, bool group) {
+  (void)K;
+  LargeMPlan p{};
+  p.group = group;
+  double best = -1.0;
+  for (int c = 0; c < kMenuSize; ++c) {
+    const TileCfg& t = kMenu[c];
+    const int BM = 32 * t.WM * t.GM, BN = 32 * t.WN * t.GN;
+    const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
+    const long tiles = (long)tm * tn;
+    const long rounds = (tiles + 255) / 256;
+    const double eff = (double)M * N / ((double)rounds * 256.0 * BM * BN);
+    const double score = eff * t.quality;
+    if (score > best + 1e-9) {
+      best = score;
+      p.cfg = c;
+      p.BM = BM;
+      p.BN = BN;
+      p.threads = 64 * t.GM * t.GN;
+      p.tiles_m = tm;
+      p.tiles_n = tn;
+    }
+  }
+  p.lds_bytes = 2 * ((size_t)p.BM * 128 + (size_t)p.BN / 16 * kBlockBytes);
+  return p;
+}
+
+hipError_t launch_largem(const LargeMPlan& p, const LargeMArgs& a, hipStream_t stream) {
+  LargeMKernel k = p.group ? pick_cfg<true>(p.cfg) : pick_cfg<false>(p.cfg);
+  if (!k) return hipErrorInvalidValue;
+  const unsigned grid = (unsigned)(p.tiles_m * p.tiles_n);
+  hipLaunchKernelGGL(k, dim3(grid), dim3(p.threads), p.lds_bytes, stream, a);
+  return hipGetLastError();
+}
+
+const char* largem_kernel_name(const LargeMPlan& p) {
+  static thread_local char buf[96];
+  snprintf(buf, sizeof buf, "largem<%dx%d,%s> tiles=%dx%d", p.BM, p.BN, p.group ? "group" : "channel",
+           p.tiles_m, p.tiles_n);
+  return buf;
+}
+
+}  // namespace w4a8

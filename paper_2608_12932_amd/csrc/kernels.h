@@ -1,0 +1,72 @@
+// Internal launch interface between the C ABI (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace w4a8 {
+
+enum OutKind { kOutBF16 = 0, kOutF32 = 1, kOutI32 = 2 };
+
+// ---- activation quantize (quantize.hip)
+hipError_t launch_quantize(const uint16_t* x, int M, int K, int8_t* q, float* scale,
+                           hipStream_t stream);
+
+// ---- weight pack (pack.hip); `err` is a device word set to 1 on a range error
+hipError_t launch_pack(const int8_t* w, int N, int K, uint8_t* out, unsigned* err,
+                       hipStream_t stream);
+hipError_t pack_error_word(unsigned** err);  // per-device status word
+
+// ---- small-M GEMM (gemm_smallm.hip)
+struct SmallMArgs {
+  const void* x;         // bf16 [M][K] (fused quantize) or int8 codes [M][K]
+  const float* x_scale;  // [M] (int8 input)
+  const uint8_t* wp;     // packed weights
+  const void* w_scale;   // fp32 [N] or fp16 [K/128][N]
+  void* y;               // [M][N]
+  void* partial;         // [S][M][N] int32 or fp32 (S > 1)
+  unsigned* counters;    // [groups] arrival counters (S > 1)
+  int M, N, K, KB;
+  int S, kbs;            // K splits and 128-k blocks per split
+  int out_kind;
+};
+struct SmallMPlan {
+  int MT, NT;            // 16-row tiles, 16-column tiles per workgroup
+  int S;                 // K splits over workgroups
+  bool fused;            // quantize inside the GEMM
+  bool group;            // group-wise scales
+  int groups;            // workgroups along N
+  size_t lds_bytes;
+};
+SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in);
+hipError_t launch_smallm(const SmallMPlan& p, const SmallMArgs& a, hipStream_t stream);
+constexpr int kSmallMWaves = 8;
+constexpr int kSmallMMaxM = 64;
+
+// ---- large-M GEMM (gemm_largem.hip)
+struct LargeMArgs {
+  const int8_t* xq;
+  const float* x_scale;
+  const uint8_t* wp;
+  const void* w_scale;
+  void* y;
+  int M, N, K, KB;
+  int out_kind;
+  int tiles_m, tiles_n;
+  int xcd_remap;
+};
+struct LargeMPlan {
+  int cfg;               // index into the tile menu
+  int BM, BN, threads;
+  bool group;
+  int tiles_m, tiles_n;
+  size_t lds_bytes;
+};
+LargeMPlan plan_largem(int M, int N, int K, bool group);
+hipError_t launch_largem(const LargeMPlan& p, const LargeMArgs& a, hipStream_t stream);
+
+const char* smallm_kernel_name(const SmallMPlan& p);
+const char* largem_kernel_name(const LargeMPlan& p);
+
+}  // namespace w4a8

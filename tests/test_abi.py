@@ -1,0 +1,97 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/w4a8.h declares, and rejects malformed calls before
+launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_12932_amd as w
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "w4a8.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(w4a8_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_names():
+    assert declared_functions() == sorted(w.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = w.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+        assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
+
+
+def test_status_strings():
+    for s in range(5):
+        assert w.status_string(s)
+    assert "unknown" in w.status_string(99)
+
+
+@pytest.mark.parametrize("N,K,want", [(24576, 4096, 24576 * 4096 // 2), (16, 128, 1024),
+                                      (4096, 12288, 4096 * 12288 // 2), (8, 128, 0), (16, 100, 0),
+                                      (16, 0, 0), (-16, 128, 0), (16, 65536 + 128, 0)])
+def test_packed_weight_bytes(N, K, want):
+    assert w.w4a8_packed_weight_bytes(N, K) == want
+
+
+def test_workspace_bytes_plans():
+    # gate+up verify: fused quantize, no split -> no workspace
+    assert w.w4a8_linear_workspace_bytes(16, 24576, 4096) == 0
+    # large M with bf16 input: codes + scales in the workspace
+    ws = w.w4a8_linear_workspace_bytes(1024, 6144, 4096)
+    assert ws >= 1024 * 4096 + 1024 * 4
+    assert w.w4a8_linear_workspace_bytes(1024, 6144, 4096, in_kind=w.IN_I8) == 0
+    # invalid shapes
+    assert w.w4a8_linear_workspace_bytes(16, 24575, 4096) == 0
+    assert w.w4a8_linear_workspace_bytes(0, 256, 256) == 0
+    assert "smallm" in w.w4a8_linear_describe(16, 24576, 4096)
+    assert "largem" in w.w4a8_linear_describe(1024, 6144, 4096)
+    assert w.w4a8_linear_describe(16, 24575, 4096) == "invalid shape"
+
+
+def test_plans_fill_the_chip():
+    # The tilings chosen for the benchmark shapes fill the 256 CUs in whole waves.
+    assert "NT=6" in w.w4a8_linear_describe(16, 24576, 4096) and "S=1 groups=256" in w.w4a8_linear_describe(16, 24576, 4096)
+    assert "tiles=8x32" in w.w4a8_linear_describe(1024, 6144, 4096)
+    d = w.w4a8_linear_describe(16, 4096, 12288)
+    assert "groups=256" in d
+
+
+def test_malformed_calls_are_rejected_without_launch():
+    L = w.lib()
+    P = ctypes.c_void_p
+    fake = P(1 << 20)  # never dereferenced: validation fails first
+    # negative M
+    assert L.w4a8_linear(fake, 0, None, -1, 256, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    # K not a multiple of 128
+    assert L.w4a8_linear(fake, 0, None, 4, 200, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    # N not a multiple of 16
+    assert L.w4a8_linear(fake, 0, None, 4, 256, fake, fake, 0, 250, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    # bad modes
+    assert L.w4a8_linear(fake, 7, None, 4, 256, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    assert L.w4a8_linear(fake, 0, None, 4, 256, fake, fake, 5, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    assert L.w4a8_linear(fake, 0, None, 4, 256, fake, fake, 0, 256, fake, 9, None, 0, None) == w.W4A8_EINVAL
+    # null / misaligned pointers
+    assert L.w4a8_linear(None, 0, None, 4, 256, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    assert L.w4a8_linear(P((1 << 20) + 8), 0, None, 4, 256, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    # int8 input without scales
+    assert L.w4a8_linear(fake, 1, None, 4, 256, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    # missing weight scales for a scaled output
+    assert L.w4a8_linear(fake, 0, None, 4, 256, fake, None, 0, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    # workspace too small (large M with bf16 input needs one)
+    assert L.w4a8_linear(fake, 0, None, 1024, 4096, fake, fake, 0, 6144, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    # M == 0 is a no-op even with null pointers
+    assert L.w4a8_linear(None, 0, None, 0, 256, None, None, 0, 256, None, 0, None, 0, None) == w.W4A8_OK
+    assert L.w4a8_quantize_act(None, 0, 256, None, None, None) == w.W4A8_OK
+    assert L.w4a8_quantize_act(fake, 4, 100, fake, fake, None) == w.W4A8_EINVAL
+    assert L.w4a8_quantize_act(None, 4, 256, fake, fake, None) == w.W4A8_EINVAL
+    assert L.w4a8_pack_weights(fake, 250, 256, fake, None) == w.W4A8_EINVAL
+    assert L.w4a8_pack_weights(None, 256, 256, fake, None) == w.W4A8_EINVAL

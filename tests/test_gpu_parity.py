@@ -1,0 +1,208 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Integer results (activation codes, scales, int32 accumulators) and the
+per-channel fp32/bf16 outputs must be bit-identical; the group-scale path,
+whose fp32 summation order is unspecified, must lie within the tolerance in
+helpers.py.  Shapes span several tiles with ragged tails on every axis, the
+workload sizes, and the degenerate cases of the method.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_12932_amd as w
+from paper_2608_12932_amd import inputs as I
+
+from helpers import (GROUP_FLOOR, NTHREADS, REL, bf16_dev, check_all_outputs, pack, run_linear,
+                     to_np_bits)
+
+pytestmark = pytest.mark.gpu
+
+
+def rng(seed):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def quant_gpu(x_bits):
+    q, s = w.w4a8_quantize_act(bf16_dev(x_bits))
+    torch.cuda.synchronize()
+    return q.cpu().numpy(), s.cpu().numpy()
+
+
+# ------------------------------------------------------------ quantize
+
+@pytest.mark.parametrize("M,K,seed", [(4, 256, 1), (16, 4096, 2), (16, 12288, 3), (1024, 4096, 4),
+                                      (3, 128, 5), (17, 640, 6), (1000, 384, 7), (2, 65536, 8)])
+def test_quantize_bit_exact(M, K, seed):
+    print(f"[case] quantize M={M} K={K} seed={seed}", flush=True)
+    x = I.activations(M, K, seed)
+    q, s = quant_gpu(x)
+    qo, so = oracle.quantize_act(x)
+    np.testing.assert_array_equal(s.view(np.uint32), so.view(np.uint32))
+    np.testing.assert_array_equal(q, qo)
+
+
+def test_quantize_special_rows():
+    print("[case] quantize special rows", flush=True)
+    K = 256
+    rows = []
+    ties = I.to_bf16_bits(np.array([127.0, 0.5, 1.5, 2.5, -2.5, 126.5, -126.5, 3.5] * (K // 8), np.float32))
+    rows.append(ties)
+    rows.append(np.zeros(K, np.uint16))                         # +0 row
+    rows.append(np.full(K, 0x8000, np.uint16))                  # -0 row
+    r = rng(9)
+    tiny = I.to_bf16_bits(r.standard_normal(K).astype(np.float32) * np.float32(1e-33))
+    rows.append(tiny)                                           # absmax below 2^-96: IEEE division path
+    denorm = r.integers(1, 0x80, K).astype(np.uint16) | (r.integers(0, 2, K).astype(np.uint16) << 15)
+    rows.append(denorm)                                         # bf16 subnormals only
+    mixed = I.activations(1, K, 10)[0].copy()
+    mixed[::7] = denorm[::7]
+    rows.append(mixed)
+    big = I.to_bf16_bits(r.standard_normal(K).astype(np.float32) * np.float32(1e30))
+    rows.append(big)
+    x = np.stack(rows)
+    q, s = quant_gpu(x)
+    qo, so = oracle.quantize_act(x)
+    np.testing.assert_array_equal(s.view(np.uint32), so.view(np.uint32))
+    np.testing.assert_array_equal(q, qo)
+    assert q[0, :8].tolist() == [127, 0, 2, 2, -2, 126, -126, 4]
+    assert not q[1].any() and not q[2].any() and s[1] == 0 and s[2] == 0
+
+
+def test_quantize_empty():
+    x = torch.empty((0, 256), dtype=torch.bfloat16, device="cuda")
+    q, s = w.w4a8_quantize_act(x)
+    assert q.shape == (0, 256) and s.shape == (0,)
+
+
+# ------------------------------------------------------------ packing
+
+@pytest.mark.parametrize("v", [1, 7, -8])
+@pytest.mark.parametrize("M", [4, 200])
+def test_one_hot_rows_select_columns(v, M):
+    # pins nibble order, sign extension of -8 and the operand lane maps of
+    # both GEMM paths
+    print(f"[case] one-hot v={v} M={M}", flush=True)
+    K, N = 512, 64
+    x = I.activations(M, K, 11)
+    r = rng(12)
+    W = np.zeros((N, K), np.int8)
+    cols = r.integers(0, K, size=N)
+    W[np.arange(N), cols] = v
+    acc = run_linear(x, pack(W), None, N, group=False, out_kind=w.OUT_I32_ACC)
+    q, _ = oracle.quantize_act(x)
+    np.testing.assert_array_equal(acc, v * q[:, cols].astype(np.int32))
+
+
+def test_pack_range_errors():
+    W = np.zeros((16, 128), np.int8)
+    W[3, 5] = 8
+    with pytest.raises(w.W4A8Error) as e:
+        pack(W)
+    assert e.value.status == w.W4A8_ERANGE
+    W[3, 5] = -9
+    with pytest.raises(w.W4A8Error):
+        pack(W)
+    W[3, 5] = -8
+    pack(W)  # in range again: the error word was cleared
+
+
+# ------------------------------------------------------------ linear, per channel
+
+SMALL_SHAPES = [(1, 256, 256), (3, 384, 64), (4, 256, 256), (16, 4096, 1024), (17, 1024, 320),
+                (33, 640, 96), (64, 512, 128), (7, 12288, 512), (16, 12288, 256)]
+
+
+@pytest.mark.parametrize("M,K,N", SMALL_SHAPES)
+@pytest.mark.parametrize("codes", [False, True])
+def test_small_m_per_channel(M, K, N, codes):
+    x = I.activations(M, K, 100 + M)
+    W, s = I.weights(N, K, 200 + N)
+    check_all_outputs(x, W, s, group=False, codes=codes, label="small-M")
+
+
+LARGE_SHAPES = [(65, 256, 320), (128, 1024, 192), (300, 640, 1040), (1024, 512, 6144), (257, 4096, 256)]
+
+
+@pytest.mark.parametrize("M,K,N", LARGE_SHAPES)
+@pytest.mark.parametrize("codes", [False, True])
+def test_large_m_per_channel(M, K, N, codes):
+    x = I.activations(M, K, 300 + M)
+    W, s = I.weights(N, K, 400 + N)
+    check_all_outputs(x, W, s, group=False, codes=codes, label="large-M")
+
+
+# ------------------------------------------------------------ linear, group scales
+
+@pytest.mark.parametrize("M,K,N", [(1, 4096, 256), (16, 1024, 384), (5, 12288, 128), (48, 512, 64),
+                                   (100, 1024, 192), (256, 1024, 1024), (513, 256, 80)])
+def test_group_scales(M, K, N):
+    x = I.activations(M, K, 500 + M)
+    W, s = I.weights(N, K, 600 + N, group=True)
+    check_all_outputs(x, W, s, group=True, label="group")
+
+
+# ------------------------------------------------------------ split-K, determinism, workspace reuse
+
+def test_split_k_paths_and_reuse():
+    # few output tiles and a long K make the planner split K across workgroups
+    for group in (False, True):
+        M, K, N = 16, 8192, 128
+        desc = w.w4a8_linear_describe(M, N, K, int(group))
+        assert "S=1 " not in desc, desc
+        x = I.activations(M, K, 700)
+        W, s = I.weights(N, K, 701, group=group)
+        ref = check_all_outputs(x, W, s, group=group, label="split-K")
+        ws = w.Workspace()
+        wp = pack(W)
+        outs = [run_linear(x, wp, s, N, group=group, out_kind=w.OUT_BF16, workspace=ws) for _ in range(20)]
+        for o in outs[1:]:
+            np.testing.assert_array_equal(o, outs[0])
+        if not group:
+            np.testing.assert_array_equal(outs[0], ref["y"])
+
+
+def test_repeat_runs_are_identical():
+    M, K, N = 1024, 4096, 6144
+    x = I.activations(M, K, 702)
+    W, s = I.weights(N, K, 703, group=True)
+    wp = pack(W)
+    first = run_linear(x, wp, s, N, group=True, out_kind=w.OUT_F32)
+    for _ in range(5):
+        np.testing.assert_array_equal(run_linear(x, wp, s, N, group=True, out_kind=w.OUT_F32).view(np.uint32),
+                                      first.view(np.uint32))
+
+
+# ------------------------------------------------------------ degenerate cases
+
+def test_zero_weights_and_zero_tokens():
+    for M in (4, 200):
+        K, N = 256, 64
+        x = I.activations(M, K, 800)
+        x[1] = 0
+        W = np.zeros((N, K), np.int8)
+        s = np.full(N, 0.01, np.float32)
+        yb = run_linear(x, pack(W), s, N, group=False, out_kind=w.OUT_BF16)
+        assert not yb.any()
+        W2, s2 = I.weights(N, K, 801)
+        yb2 = run_linear(x, pack(W2), s2, N, group=False, out_kind=w.OUT_BF16)
+        assert not yb2[1].any()
+
+
+def test_empty_batch():
+    wp = pack(np.zeros((64, 256), np.int8))
+    x = torch.empty((0, 256), dtype=torch.bfloat16, device="cuda")
+    y = w.w4a8_linear(x, wp, torch.ones(64, device="cuda"), 64)
+    assert y.shape == (0, 64)
+
+
+def test_minimum_and_extreme_shapes():
+    # smallest legal layer, and the closed-form extreme: x = +-1, W = -8
+    for M, K, N in ((1, 128, 16), (2, 12288, 16)):
+        xs = np.stack([I.to_bf16_bits(np.ones(K, np.float32)), I.to_bf16_bits(-np.ones(K, np.float32))])[:M]
+        W = np.full((N, K), -8, np.int8)
+        acc = run_linear(xs, pack(W), None, N, group=False, out_kind=w.OUT_I32_ACC)
+        assert (acc[0] == -1016 * K).all()
+        if M > 1:
+            assert (acc[1] == 1016 * K).all()

@@ -1,0 +1,310 @@
+"""Benchmark of the W4A8 linear layer on one MI355X.
+
+A step is one full pass of the hot path, y = dequant(quant8(x) . int4(W)^T):
+activation quantize, packed-int4 weight stream and int8 MFMA contraction,
+dequant epilogue, bf16 out, with every input already resident in HBM.
+
+Primary line: draft-block verification of the fused gate+up projection,
+M=16 tokens, K=4096, N=24576 (bandwidth bound, reported in GB/s of
+algorithmic bytes: packed weights + weight scales + bf16 x + bf16 y).
+Eight copies of the packed weight (403 MB, more than the 256 MB on-die
+Infinity Cache) are cycled so every step streams its weights from HBM.
+
+Secondary object: streaming prefill of new-frame tokens through the fused
+QKV projection, M=1024, K=4096, N=6144 (MFMA bound, reported in INT8 TOPS,
+2*M*N*K ops per step), cycling 24 weight copies.
+
+Timing: W untimed warmup steps, then exactly K steps between HIP events on
+the launch stream, bracketed by device synchronization.  The dominant
+kernel's average duration for the roofline is timed the same way over its
+own back-to-back launches.  The CPU baseline times the oracle (test
+infrastructure, plain scalar C) on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "W4A8 linear: HBM GB/s at M=16, INT8 TOPS at M=1024 (% of roofline)"
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+INT8_PEAK_TOPS = 5000.0      # MI355X dense INT8 MFMA (5.0 POPS)
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ["device.h", "gemm_smallm.hip", "gemm_largem.hip", "quantize.hip", "api.cpp"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_12932_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(name: str):
+    """HBM bytes per dispatch from a committed rocprofv3 counter summary, or
+    None if there is none or the kernels changed since it was taken."""
+    path = os.path.join(PROFILES, f"{name}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_dispatch"])
+    except (KeyError, ValueError):
+        return None
+
+
+class DirectCall:
+    """w4a8_linear with every argument resolved once (device pointers and
+    sizes), so a step costs one C call: the binding's per-call tensor checks
+    would otherwise dominate a ~10 us kernel."""
+
+    def __init__(self, x, wps, w_scale, N, y, x_scale=None, workspace=None, out_kind=0):
+        import ctypes
+        import paper_2608_12932_amd as w
+
+        self.L = w.lib()
+        self.M, self.K = x.shape
+        self.in_kind = w.IN_I8 if x.dtype.is_floating_point is False else w.IN_BF16
+        self.x = x.data_ptr()
+        self.xs = None if x_scale is None else x_scale.data_ptr()
+        self.wps = [t.data_ptr() for t in wps]
+        self.ws = w_scale.data_ptr()
+        self.N = N
+        self.y = y.data_ptr()
+        self.out_kind = out_kind
+        need = w.w4a8_linear_workspace_bytes(self.M, N, self.K, w.SCALE_CHANNEL_F32, self.in_kind)
+        self.wk = None
+        self.wk_bytes = 0
+        if need:
+            buf = workspace.get(need)
+            self.wk, self.wk_bytes = buf.data_ptr(), buf.numel()
+        self.keep = (x, wps, w_scale, y, x_scale, workspace)
+        self.c_size = ctypes.c_size_t
+
+    def __call__(self, i, stream):
+        rc = self.L.w4a8_linear(self.x, self.in_kind, self.xs, self.M, self.K, self.wps[i % len(self.wps)],
+                                self.ws, 0, self.N, self.y, self.out_kind, self.wk, self.wk_bytes, stream)
+        if rc:
+            raise RuntimeError(f"w4a8_linear failed: {rc}")
+
+
+def time_direct(call, steps: int, warmup: int):
+    import torch
+
+    stream = torch.cuda.current_stream().cuda_stream
+    return time_steps(lambda i: call(i, stream), steps, warmup)
+
+
+def time_graph(call, steps: int, warmup: int):
+    """The same K steps captured once in a HIP graph and replayed."""
+    import torch
+
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        for i in range(warmup):
+            call(i, side.cuda_stream)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        st = torch.cuda.current_stream().cuda_stream
+        for i in range(steps):
+            call(i, st)
+    g.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def time_steps(fn, steps: int, warmup: int):
+    import torch
+
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        fn(i)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps  # ms per step
+
+
+def gate_up_setup(copies=16):
+    import torch
+    import paper_2608_12932_amd as w
+    from paper_2608_12932_amd import inputs as I
+
+    x, W, s, K, N = I.workload_inputs("gate_up_verify", 16)
+    dev = torch.device("cuda:0")
+    xd = torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+    wp0 = w.w4a8_pack_weights(torch.from_numpy(W).to(dev))
+    wps = [wp0] + [wp0.clone() for _ in range(copies - 1)]
+    sd = torch.from_numpy(s).to(dev)
+    y = torch.empty((16, N), dtype=torch.bfloat16, device=dev)
+    ws = w.Workspace(dev)
+    return dict(x=x, W=W, s=s, xd=xd, wps=wps, sd=sd, y=y, ws=ws, M=16, K=K, N=N)
+
+
+def bench_gate_up(steps, warmup):
+    import paper_2608_12932_amd as w
+
+    d = gate_up_setup()
+    M, K, N = d["M"], d["K"], d["N"]
+    wps, xd, sd, y, ws = d["wps"], d["xd"], d["sd"], d["y"], d["ws"]
+
+    def step(i):
+        w.w4a8_linear(xd, wps[i % len(wps)], sd, N, out=y, workspace=ws)
+
+    ms = time_steps(step, steps, warmup)
+    algo_bytes = N * K // 2 + N * 4 + M * K * 2 + M * N * 2
+    return d, ms, algo_bytes
+
+
+def qkv_setup(copies=24):
+    import torch
+    import paper_2608_12932_amd as w
+    from paper_2608_12932_amd import inputs as I
+
+    x, W, s, K, N = I.workload_inputs("qkv_prefill", 1024)
+    dev = torch.device("cuda:0")
+    xd = torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+    wp0 = w.w4a8_pack_weights(torch.from_numpy(W).to(dev))
+    wps = [wp0] + [wp0.clone() for _ in range(copies - 1)]
+    sd = torch.from_numpy(s).to(dev)
+    y = torch.empty((1024, N), dtype=torch.bfloat16, device=dev)
+    return dict(xd=xd, wps=wps, sd=sd, y=y, ws=w.Workspace(dev), M=1024, K=K, N=N)
+
+
+def bench_qkv(steps, warmup):
+    import paper_2608_12932_amd as w
+
+    d = qkv_setup()
+    M, K, N = d["M"], d["K"], d["N"]
+    wps, xd, sd, y, ws = d["wps"], d["xd"], d["sd"], d["y"], d["ws"]
+
+    def step(i):
+        w.w4a8_linear(xd, wps[i % len(wps)], sd, N, out=y, workspace=ws)
+
+    ms_step = time_steps(step, steps, warmup)
+    # the dominant kernel alone: the GEMM on pre-quantized codes
+    q, sx = w.w4a8_quantize_act(xd)
+
+    def gemm(i):
+        w.w4a8_linear(q, wps[i % len(wps)], sd, N, x_scale=sx, out=y)
+
+    ms_gemm = time_steps(gemm, steps, warmup)
+
+    def quant(i):
+        w.w4a8_quantize_act(xd)
+
+    ms_quant = time_steps(quant, steps, warmup)
+    ops = 2 * M * N * K
+    return dict(M=M, K=K, N=N, ms_step=ms_step, ms_gemm=ms_gemm, ms_quant=ms_quant, ops=ops)
+
+
+def cpu_baseline(d, algo_bytes, reps=3):
+    import oracle
+
+    threads = min(d["M"], len(os.sched_getaffinity(0)))
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        oracle.linear(d["x"], d["W"], s_w=d["s"], nthreads=threads)
+        times.append(time.perf_counter() - t0)
+    t = statistics.median(times)
+    return {"value": round(algo_bytes / t / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"the full gate+up verify layer (M=16 K=4096 N=24576: quantize, int64 contraction, "
+                      f"dequant), median of {reps} runs, {t:.2f} s each"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the layer would shard by output columns or by K; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_12932_amd as w
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w.lib()
+    d, ms, algo_bytes = bench_gate_up(args.steps, args.warmup)
+    gbs = algo_bytes / (ms * 1e-3) / 1e9
+    M, K, N = d["M"], d["K"], d["N"]
+    traffic = counter_traffic("smallm_gate_up_verify")
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": "gate+up verify (fused gate+up projection, draft-block verification)",
+                   "M": M, "K": K, "N": N, "scales": "per-channel fp32", "x": "bf16 in, quantized in-call",
+                   "y": "bf16", "weight_copies": len(d["wps"]), "algorithmic_bytes": algo_bytes},
+        "kernel": w.w4a8_linear_describe(M, N, K),
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
+    }
+    if not args.no_secondary:
+        r = bench_qkv(max(50, args.steps // 5), max(10, args.warmup // 5))
+        tops_step = r["ops"] / (r["ms_step"] * 1e-3) / 1e12
+        tops_gemm = r["ops"] / (r["ms_gemm"] * 1e-3) / 1e12
+        out["secondary"] = {
+            "metric": "INT8 TOPS at M=1024 (qkv prefill)",
+            "value": round(tops_step, 2),
+            "unit": "TOPS",
+            "ms_per_step": round(r["ms_step"], 6),
+            "config": {"workload": "qkv prefill (fused QKV projection, streaming prefill of new-frame tokens)",
+                       "M": r["M"], "K": r["K"], "N": r["N"], "scales": "per-channel fp32",
+                       "x": "bf16 in, quantized by its own kernel", "y": "bf16", "weight_copies": 24},
+            "kernel": w.w4a8_linear_describe(r["M"], r["N"], r["K"]),
+            "quantize_ms": round(r["ms_quant"], 6),
+            "roofline": {"bound": "mfma", "achieved": round(tops_gemm, 2), "peak": INT8_PEAK_TOPS, "unit": "TOPS",
+                         "frac": round(tops_gemm / INT8_PEAK_TOPS, 4), "gemm_ms": round(r["ms_gemm"], 6),
+                         "traffic": counter_traffic("largem_qkv_prefill")},
+        }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(d, algo_bytes)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -110,7 +110,7 @@ size_t w4a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mo
   if (M < 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return 0;
   if (scale_mode != W4A8_SCALE_CHANNEL_F32 && scale_mode != W4A8_SCALE_GROUP_F16) return 0;
   if (in_kind != W4A8_IN_BF16 && in_kind != W4A8_IN_I8) return 0;
-  if (M == 0) return 0;
+  if (M == 0 || (uint64_t)N * (uint64_t)K >= (uint64_t(1) << 37)) return 0;
   return make_plan(M, N, K, scale_mode == W4A8_SCALE_GROUP_F16, in_kind == W4A8_IN_BF16).total;
 }
 
@@ -142,6 +142,8 @@ w4a8_status w4a8_linear(const void* x, int in_kind, const float* x_scale, int64_
   if (out_kind != W4A8_OUT_BF16 && out_kind != W4A8_OUT_F32 && out_kind != W4A8_OUT_I32_ACC)
     return W4A8_EINVAL;
   if (M == 0) return W4A8_OK;
+  // 32-bit buffer offsets: the group-scale array (N*K/64 bytes) stays below 2 GiB
+  if ((uint64_t)N * (uint64_t)K >= (uint64_t(1) << 37)) return W4A8_EUNSUPPORTED;
   if (!x || !aligned(x, 16) || !w_packed || !aligned(w_packed, 16) || !y || !aligned(y, 16))
     return W4A8_EINVAL;
   if (in_kind == W4A8_IN_I8 && (!x_scale || !aligned(x_scale, 4))) return W4A8_EINVAL;
@@ -173,7 +175,10 @@ w4a8_status w4a8_linear(const void* x, int in_kind, const float* x_scale, int64_
   if (p.small_m) {
     SmallMPlan sm = p.sm;
     sm.group = group;
-    if (!sm.fused || !bf16_in) sm.fused = false;
+    if (!bf16_in) {
+      sm.fused = false;
+      sm.qmode = 0;
+    }
     SmallMArgs a{};
     a.x = xin;
     a.x_scale = sx;
@@ -188,6 +193,7 @@ w4a8_status w4a8_linear(const void* x, int in_kind, const float* x_scale, int64_
     a.KB = (int)(K / W4A8_GROUP_SIZE);
     a.S = sm.S;
     a.kbs = (a.KB + sm.S - 1) / sm.S;
+    a.tpr = sm.tpr;
     a.out_kind = out_kind;
     e = launch_smallm(sm, a, stream);
   } else {

@@ -194,4 +194,48 @@ __device__ __forceinline__ uint4 ldg_nt(const uint4* p) {
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
+// ---- buffer loads
+// A raw buffer resource covers `bytes` bytes from `base`; a load whose
+// offset lies at or beyond that range returns zeros without touching memory.
+// Tails and padding are therefore expressed as out-of-range offsets instead
+// of branches: a guarded load would otherwise become a branch whose join
+// forces the wave to wait for the load right away, serializing the stream.
+constexpr uint32_t kOOB = 0x80000000u;       // offset beyond any range used here
+constexpr int kCacheDefault = 0;
+constexpr int kCacheStream = 2;              // non-temporal: read once, do not keep
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+template <int kAux = kCacheDefault>
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const v4i v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kAux);
+  return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
+}
+
+// Same with a wave-uniform scalar offset added to the address.  Range checks
+// apply to the vector offset, so an out-of-range vector offset still reads
+// zeros; in-range vector offsets are only ever paired with scalar offsets
+// that keep the address inside the resource.
+template <int kAux = kCacheDefault>
+__device__ __forceinline__ uint4 buf_load16s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  const v4i v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, kAux);
+  return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
+}
+template <int kAux = kCacheDefault>
+__device__ __forceinline__ uint16_t buf_load2s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return (uint16_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)soff, kAux);
+}
+
+template <int kAux = kCacheDefault>
+__device__ __forceinline__ uint16_t buf_load2(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return (uint16_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, kAux);
+}
+
+template <int kAux = kCacheDefault>
+__device__ __forceinline__ uint32_t buf_load4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, kAux);
+}
+
 }  // namespace w4a8

@@ -52,24 +52,32 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   const int ntiles = N / 16;
   const int l32 = lane & 31, g2 = lane >> 5;
 
+  // Per-tile buffer resources: rows past M and tiles past N lie outside
+  // them and read as zeros (no branch, no traffic).
+  const int rows_here = min(BM, M - m0);
+  const int tiles_here = min(BN / 16, ntiles - nt0);
+  const __amdgpu_buffer_rsrc_t ares = make_rsrc(a.xq + (size_t)m0 * K, (uint32_t)(rows_here * K));
+  const __amdgpu_buffer_rsrc_t bres =
+      make_rsrc(a.wp + (size_t)nt0 * KB * kBlockBytes, (uint32_t)(tiles_here * KB * kBlockBytes));
+  const int cols_here = min(BN, N - n0);
+  const __amdgpu_buffer_rsrc_t sres =
+      make_rsrc(static_cast<const uint16_t*>(a.w_scale) + n0, (uint32_t)(((size_t)KB * N - n0) * 2));
+
   uint4 ra[kACh], rb[kBCh];
+  // kb == KB (the prefetch after the last step) loads nothing.
   auto gload = [&](int kb) {
+    const bool ok = kb < KB;
 #pragma unroll
     for (int i = 0; i < kACh; ++i) {
       const int idx = tid + i * kThreads;
       const int row = idx >> 3, ch = idx & 7;
-      const int grow = m0 + row;
-      ra[i] = grow < M ? *reinterpret_cast<const uint4*>(a.xq + (size_t)grow * K + kb * 128 + ch * 16)
-                       : make_uint4(0, 0, 0, 0);
+      ra[i] = buf_load16(ares, ok ? (uint32_t)(row * K + kb * 128 + ch * 16) : kOOB);
     }
 #pragma unroll
     for (int i = 0; i < kBCh; ++i) {
       const int idx = tid + i * kThreads;
       const int blk = idx >> 6, j = idx & 63;
-      const int tile = nt0 + blk;
-      rb[i] = tile < ntiles
-                  ? ldg_nt(reinterpret_cast<const uint4*>(a.wp + ((size_t)tile * KB + kb) * kBlockBytes) + j)
-                  : make_uint4(0, 0, 0, 0);
+      rb[i] = buf_load16<kCacheStream>(bres, ok ? (uint32_t)((blk * KB + kb) * kBlockBytes + j * 16) : kOOB);
     }
   };
   auto swrite = [&](int buf) {
@@ -106,14 +114,13 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   __syncthreads();
   for (int kb = 0; kb < KB; ++kb) {
     const int buf = kb & 1;
-    if (kb + 1 < KB) gload(kb + 1);
-    float sg[GROUP ? WN : 1];
+    gload(kb + 1);
+    uint16_t sgr[GROUP ? WN : 1];
     if constexpr (GROUP) {
-      const uint16_t* sgp = static_cast<const uint16_t*>(a.w_scale);
 #pragma unroll
       for (int j = 0; j < WN; ++j) {
-        const int col = n0 + wn * 32 * WN + j * 32 + l32;
-        sg[j] = col < N ? f16_to_f32(sgp[(size_t)kb * N + col]) * 0.0625f : 0.0f;
+        const int col = wn * 32 * WN + j * 32 + l32;
+        sgr[j] = buf_load2(sres, col < cols_here ? (uint32_t)(((size_t)kb * N + col) * 2) : kOOB);
       }
 #pragma unroll
       for (int i = 0; i < WM; ++i)
@@ -156,35 +163,46 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
         for (int j = 0; j < WN; ++j)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) facc[i][j][r] = __fmaf_rn((float)acc[i][j][r], sg[j], facc[i][j][r]);
+          for (int r = 0; r < 16; ++r)
+            facc[i][j][r] = __fmaf_rn((float)acc[i][j][r], f16_to_f32(sgr[j]) * 0.0625f, facc[i][j][r]);
     }
-    if (kb + 1 < KB) swrite(buf ^ 1);
+    swrite(buf ^ 1);  // after the last step this fills the idle half with zeros
     __syncthreads();
   }
 
   // ---- epilogue: lane holds column l32, rows 8 (r / 4) + 4 g2 + r % 4
+  const bool scaled = a.out_kind != kOutI32;
+  const __amdgpu_buffer_rsrc_t xsres = make_rsrc(a.x_scale + m0, scaled ? (uint32_t)(rows_here * 4) : 0u);
+  const __amdgpu_buffer_rsrc_t wsres =
+      make_rsrc(static_cast<const float*>(a.w_scale) + n0, (!GROUP && scaled) ? (uint32_t)(cols_here * 4) : 0u);
+  float swv[WN];
+#pragma unroll
+  for (int j = 0; j < WN; ++j)
+    swv[j] = __uint_as_float(buf_load4(wsres, (uint32_t)((wn * 32 * WN + j * 32 + l32) * 4)));
 #pragma unroll
   for (int i = 0; i < WM; ++i) {
+    float sxv[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      sxv[r] = __uint_as_float(buf_load4(xsres, (uint32_t)((wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3)) * 4)));
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = m0 + wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3);
-      if (row >= M) continue;
-      const float sx = a.out_kind == kOutI32 ? 0.0f : a.x_scale[row];
 #pragma unroll
       for (int j = 0; j < WN; ++j) {
         const int col = n0 + wn * 32 * WN + j * 32 + l32;
-        if (col >= N) continue;
+        if (row >= M || col >= N) continue;
         const size_t o = (size_t)row * N + col;
         float y32;
         if constexpr (GROUP) {
-          y32 = __fmul_rn(facc[i][j][r], sx);
+          y32 = __fmul_rn(facc[i][j][r], sxv[r]);
         } else {
           const int v = acc[i][j][r] >> 4;
-          if (a.out_kind == kOutI32) {
+          if (!scaled) {
             static_cast<int*>(a.y)[o] = v;
             continue;
           }
-          y32 = __fmul_rn(__fmul_rn((float)v, sx), static_cast<const float*>(a.w_scale)[col]);
+          y32 = __fmul_rn(__fmul_rn((float)v, sxv[r]), swv[j]);
         }
         if (a.out_kind == kOutF32)
           static_cast<float*>(a.y)[o] = y32;

@@ -12,10 +12,15 @@
 //   - the partial sums of the 8 waves are reduced through LDS, and K splits
 //     across workgroups (S > 1) meet in a workspace, where the last arriving
 //     workgroup of a column group sums them in split order and finishes;
-//   - with bf16 input and a small enough M*K, the per-token quantize is fused
-//     in front: every workgroup reads the whole token rows (from L2) for the
-//     absmax, then quantizes only its own K split into LDS, while its first
-//     weight loads are already in flight.
+//   - with bf16 input the per-token quantize is fused in front, in one of two
+//     ways.  Register mode (one K split, at most 4 blocks per wave): each lane
+//     loads exactly the bf16 values its own A fragments need, the row maxima
+//     meet through two shuffles and one LDS atomic per row, and each lane
+//     quantizes its values in registers; the 8 waves read the activations
+//     once per workgroup.  LDS mode (longer K or several splits): every
+//     workgroup reads the whole token rows for the absmax and quantizes its
+//     own split into LDS, which the waves then read.  In both, the weight
+//     stream is already in flight while the codes are made.
 // The epilogue applies the per-token and per-channel (or per-group) scales.
 #include <cstdio>
 
@@ -29,39 +34,47 @@ namespace {
 constexpr int kWaves = kSmallMWaves;
 constexpr int kThreads = kWaves * 64;
 constexpr int kXCache = 16;       // fused quantize: x chunks held per thread
-constexpr int kOperandVgprs = 112;
+constexpr int kOperandVgprs = 128;   // registers for in-flight weight (+ activation) stages
+constexpr int kOperandVgprsFused = 112;  // the fused path also holds the x chunks
 constexpr int kLdsHeader = 256;   // per-row absmax / s / inv / mode
 constexpr int kMaxTilesPerWave = 12;
+constexpr int kMaxGroupTiles = 3;  // int8-input group kernels: more tiles spill
+constexpr int kMaxFusedTiles = 2;  // fused quantize pays off up to this many tiles
 
-template <int MT, int NT, bool FUSED>
+// How the activations reach the MFMA A operand.
+enum QMode {
+  kQNone = 0,  // int8 codes from memory (x_scale given)
+  kQLds = 1,   // bf16 in; codes made in LDS
+};
+
+template <int MT, int NT, int QM>
 constexpr int stage_depth() {
-  int per = NT * 4 + (FUSED ? 0 : MT * 8);
-  int d = kOperandVgprs / per;
+  int per = NT * 4 + (QM == kQLds ? 0 : MT * 8);
+  int d = (QM == kQLds ? kOperandVgprsFused : kOperandVgprs) / per;
   return d < 1 ? 1 : (d > 16 ? 16 : d);
 }
 
+// Output of one element from its reduced accumulator.
 struct Emit {
   const SmallMArgs& a;
-  const float* lds_scale;  // fused: per-row s in LDS; else nullptr
-  __device__ float sx(int row) const { return lds_scale ? lds_scale[row] : a.x_scale[row]; }
   // per-channel: v = 16 * acc
-  __device__ void channel(int row, int n, int v) const {
+  __device__ void channel(int row, int n, int v, float sx, float sw) const {
     const size_t o = (size_t)row * a.N + n;
     const int acc = v >> 4;
     if (a.out_kind == kOutI32) {
       static_cast<int*>(a.y)[o] = acc;
       return;
     }
-    const float y32 = __fmul_rn(__fmul_rn((float)acc, sx(row)), static_cast<const float*>(a.w_scale)[n]);
+    const float y32 = __fmul_rn(__fmul_rn((float)acc, sx), sw);
     if (a.out_kind == kOutF32)
       static_cast<float*>(a.y)[o] = y32;
     else
       static_cast<uint16_t*>(a.y)[o] = (uint16_t)f32_to_bf16(y32);
   }
   // group: t = sum_g p_g * s_g
-  __device__ void group(int row, int n, float t) const {
+  __device__ void group(int row, int n, float t, float sx) const {
     const size_t o = (size_t)row * a.N + n;
-    const float y32 = __fmul_rn(t, sx(row));
+    const float y32 = __fmul_rn(t, sx);
     if (a.out_kind == kOutF32)
       static_cast<float*>(a.y)[o] = y32;
     else
@@ -69,9 +82,10 @@ struct Emit {
   }
 };
 
-template <int MT, int NT, bool GROUP, bool FUSED>
+template <int MT, int NT, bool GROUP, int QM>
 __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
-  constexpr int D = stage_depth<MT, NT, FUSED>();
+  constexpr bool FUSED = QM != kQNone;
+  constexpr int D = stage_depth<MT, NT, QM>();
   extern __shared__ __align__(16) uint8_t lds[];
   uint32_t* l_amax = reinterpret_cast<uint32_t*>(lds);
   float* l_s = reinterpret_cast<float*>(lds + 64);
@@ -80,7 +94,8 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   uint8_t* l_body = lds + kLdsHeader;
   __shared__ int l_last;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int gid = blockIdx.x / a.S, split = blockIdx.x % a.S;
   const int M = a.M, N = a.N, K = a.K, KB = a.KB;
   const int ntiles = N / 16;
@@ -88,77 +103,109 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   const int kb_begin = split * a.kbs;
   const int kb_end = min(KB, kb_begin + a.kbs);
   const int nkb = kb_end - kb_begin;
-  const int iters = wave < nkb ? (nkb - wave + kWaves - 1) / kWaves : 0;
+  // Uniform trip count: stages past the end of the split load zeros.
+  const int iters = (nkb + kWaves - 1) / kWaves;
   const int r16 = lane & 15, g4 = lane >> 4;
   const int ldq = nkb * 128 + 16;  // fused: LDS row stride of the codes
 
-  // ---- fused quantize: load this thread's x chunks first (so that waiting
-  // for them later does not wait for the weight stream issued after them)
-  uint4 xc[FUSED ? kXCache : 1];
-  int cpr = 1, nx = 0;
-  if constexpr (FUSED) {
-    cpr = (K / 8) / kThreads;
-    nx = M * cpr;
-    const uint4* xg = static_cast<const uint4*>(a.x);
+  // The NT tiles of this group are contiguous in the packed layout; tiles
+  // past N fall outside the resource and read as zeros.
+  const int tiles_here = min(NT, ntiles - nt0);
+  const __amdgpu_buffer_rsrc_t wres =
+      make_rsrc(a.wp + (size_t)nt0 * KB * kBlockBytes, (uint32_t)(tiles_here * KB * kBlockBytes));
+  const __amdgpu_buffer_rsrc_t sres =
+      GROUP ? make_rsrc(static_cast<const uint16_t*>(a.w_scale) + nt0 * 16,
+                        (uint32_t)(((size_t)KB * N - nt0 * 16) * 2))
+            : wres;
+  const __amdgpu_buffer_rsrc_t xres = make_rsrc(a.x, (uint32_t)((size_t)M * K * (FUSED ? 2 : 1)));
+
+  // ---- fused quantize: load this thread's x chunks first, so that waiting
+  // for them later does not wait for the weight stream issued after them.
+  // Thread tid owns row tid / tpr and, of that row's K/8 16-byte chunks,
+  // c8 = tid % tpr + tpr * j; chunks past the row read as zeros.
+  // Every workgroup reads the rows in the same order: concurrent requests
+  // for the same line then merge in L2.
+  uint4 xc[QM == kQLds ? kXCache : 1];
+  const int tpr = QM == kQLds ? a.tpr : 1;
+  const int xrow = tid / tpr, xcol = tid % tpr;
+  const int nchunk = K / 8;                  // a multiple of tpr (host-side condition)
+  const int cpt = nchunk / tpr;              // chunk slots used per thread (<= kXCache)
+  auto xchunk = [&](int j) { return xcol + tpr * j; };
+  if constexpr (QM == kQLds) {
+    // one vector offset per thread; the chunk step goes in the scalar offset
+    const uint32_t xbase = xrow < M ? (uint32_t)((xrow * nchunk + xcol) * 16) : kOOB;
 #pragma unroll
     for (int j = 0; j < kXCache; ++j)
-      if (j < nx) xc[j] = xg[(size_t)j * kThreads + tid];
+      xc[j] = buf_load16s(xres, j < cpt ? xbase : kOOB, (uint32_t)(j * tpr * 16));
     if (tid < 16) l_amax[tid] = 0u;
   }
 
-  // ---- weight stream, D blocks deep
+  // ---- weight stream, D stages deep
   uint4 wb[D][NT];
   uint4 ab[FUSED ? 1 : D][MT][2];
-  float sgb[GROUP ? D : 1][NT];
-  const uint8_t* wp = a.wp;
+  uint16_t sgb[GROUP ? D : 1][NT];
+  // Stage i of this wave covers block kb_begin + wave + 8 i of the split.
+  auto stage_kb = [&](int i) { return kb_begin + wave + i * kWaves; };
+  // The wave-uniform part of each offset (tile, block) goes in the scalar
+  // offset; the lane part, or an out-of-range value, in the vector offset.
   auto load_stage = [&](int slot, int i) {
-    const int kb = kb_begin + wave + i * kWaves;
+    const int kb = stage_kb(i);
+    const bool ok = kb < kb_end;
+    const uint32_t wv = ok ? (uint32_t)(lane * 16) : kOOB;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      const int tile = nt0 + t;
-      wb[slot][t] = tile < ntiles
-                        ? ldg_nt(reinterpret_cast<const uint4*>(wp + ((size_t)tile * KB + kb) * kBlockBytes) + lane)
-                        : make_uint4(0, 0, 0, 0);
-      if constexpr (GROUP) {
-        const uint16_t* sg = static_cast<const uint16_t*>(a.w_scale);
-        sgb[slot][t] = tile < ntiles ? f16_to_f32(sg[(size_t)kb * N + tile * 16 + r16]) * 0.0625f : 0.0f;
-      }
+      wb[slot][t] = buf_load16s<kCacheStream>(wres, wv, (uint32_t)((t * KB + (ok ? kb : 0)) * kBlockBytes));
+      if constexpr (GROUP)
+        sgb[slot][t] = buf_load2s(sres, ok ? (uint32_t)((t * 16 + r16) * 2) : kOOB, (uint32_t)((size_t)(ok ? kb : 0) * N * 2));
     }
     if constexpr (!FUSED) {
-      const int8_t* xq = static_cast<const int8_t*>(a.x);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int row = mt * 16 + r16;
-        if (row < M) {
-          const uint4* p = reinterpret_cast<const uint4*>(xq + (size_t)row * K + kb * 128 + g4 * 32);
-          ab[slot][mt][0] = p[0];
-          ab[slot][mt][1] = p[1];
-        } else {
-          ab[slot][mt][0] = make_uint4(0, 0, 0, 0);
-          ab[slot][mt][1] = make_uint4(0, 0, 0, 0);
-        }
+        const uint32_t off = ok && row < M ? (uint32_t)(row * K + g4 * 32) : kOOB;
+        const uint32_t so = (uint32_t)((ok ? kb : 0) * 128);
+        ab[slot][mt][0] = buf_load16s(xres, off, so);
+        ab[slot][mt][1] = buf_load16s(xres, off == kOOB ? kOOB : off + 16, so);
       }
     }
   };
+  // Without the LDS-mode quantize the whole prologue is issued at once.
+  if constexpr (QM != kQLds) {
 #pragma unroll
-  for (int s = 0; s < D; ++s)
-    if (s < iters) load_stage(s, s);
+    for (int s = 0; s < D; ++s) load_stage(s, s);
+  }
 
-  // ---- fused quantize: absmax over the full rows, codes for this split
-  if constexpr (FUSED) {
+  // ---- epilogue scales, fetched now so their latency hides under the
+  // weight stream.  Thread tid finishes outputs o = tid + q * threads.
+  constexpr int kOut = MT * 16 * NT * 16;
+  constexpr int kOPT = (kOut + kThreads - 1) / kThreads;
+  const bool scaled = a.out_kind != kOutI32;
+  const __amdgpu_buffer_rsrc_t swres =
+      make_rsrc(static_cast<const float*>(a.w_scale) + nt0 * 16, !GROUP && scaled ? (uint32_t)(tiles_here * 64) : 0u);
+  const __amdgpu_buffer_rsrc_t sxres = make_rsrc(a.x_scale, !FUSED && scaled ? (uint32_t)(M * 4) : 0u);
+  float swp[kOPT], sxp[kOPT];
+#pragma unroll
+  for (int q = 0; q < kOPT; ++q) {
+    const int o = tid + q * kThreads;
+    const int row = o / (NT * 16), col = o % (NT * 16);
+    const bool ok = o < kOut && row < M;
+    swp[q] = __uint_as_float(buf_load4(swres, ok ? (uint32_t)(col * 4) : kOOB));
+    sxp[q] = __uint_as_float(buf_load4(sxres, ok ? (uint32_t)(row * 4) : kOOB));
+  }
+
+  // ---- LDS-mode quantize: absmax over the full rows, codes for this split
+  if constexpr (QM == kQLds) {
     lds_barrier();  // l_amax initialised
     uint32_t pm = 0;
 #pragma unroll
-    for (int j = 0; j < kXCache; ++j) {
-      if (j < nx) {
-        pm = absmax_chunk(pm, xc[j]);
-        if ((j + 1) % cpr == 0) {
-          const uint32_t v = wave_max_u32(fold_pair_max(pm));
-          if (lane == 0) atomicMax(&l_amax[j / cpr], v);
-          pm = 0;
-        }
-      }
+    for (int j = 0; j < kXCache; ++j) pm = absmax_chunk(pm, xc[j]);
+    uint32_t v = fold_pair_max(pm);
+    const int width = tpr < 64 ? tpr : 64;  // lanes of one row within a wave
+    for (int off = width / 2; off >= 1; off >>= 1) {
+      const uint32_t o = (uint32_t)__shfl_xor((int)v, off, 64);
+      v = v > o ? v : o;
     }
+    if (xrow < M && (lane & (width - 1)) == 0) atomicMax(&l_amax[xrow], v);
     lds_barrier();
     if (tid < M) {
       const QScale q = qscale_from_absmax(bf16_lo(l_amax[tid]));
@@ -167,18 +214,30 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
       l_mode[tid] = q.mode;
     }
     lds_barrier();
+    // The activation rows came in alone (the weight stream would have
+    // queued them behind it).  Now start the weight stream one stage at a
+    // time, quantizing a share of the chunks between stages: a wave that
+    // issued its whole prologue at once would sit blocked on the memory
+    // pipeline with its quantize work still ahead of it.
+    const float qs = xrow < M ? l_s[xrow] : 0.0f, qinv = xrow < M ? l_inv[xrow] : 0.0f;
+    const int qmode = xrow < M ? l_mode[xrow] : 0;
     const int k_lo = kb_begin * 128, k_hi = kb_end * 128;
+    uint8_t* dst = l_body + min(xrow, M - 1) * ldq - k_lo;
+    constexpr int kPer = (kXCache + D - 1) / D;  // chunks quantized after each stage
 #pragma unroll
-    for (int j = 0; j < kXCache; ++j) {
-      if (j < nx) {
-        const int row = j / cpr;
-        const int k = ((j % cpr) * kThreads + tid) * 8;
-        if (k >= k_lo && k < k_hi) {
-          const int mode = __builtin_amdgcn_readfirstlane(l_mode[row]);
-          const uint2 o = quant_chunk(xc[j], l_s[row], l_inv[row], mode);
-          *reinterpret_cast<uint2*>(l_body + row * ldq + (k - k_lo)) = o;
+    for (int st = 0; st < D; ++st) {
+      load_stage(st, st);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int jj = 0; jj < kPer; ++jj) {
+        const int j = st * kPer + jj;
+        if (j < kXCache) {
+          const int k = xchunk(j) * 8;
+          if (xrow < M && j < cpt && k >= k_lo && k < k_hi)  // k < K since j < cpt
+            *reinterpret_cast<uint2*>(dst + k) = quant_chunk(xc[j], qs, qinv, qmode);
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
     lds_barrier();
   }
@@ -201,44 +260,40 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
 #pragma unroll
     for (int s = 0; s < D; ++s) {
       const int i = base + s;
-      if (i < iters) {
-        v4i alo[MT], ahi[MT];
-        if constexpr (FUSED) {
-          if (r16 < M) {
-            const int kb = kb_begin + wave + i * kWaves;
-            const uint8_t* p = l_body + r16 * ldq + (kb - kb_begin) * 128 + g4 * 32;
-            alo[0] = *reinterpret_cast<const v4i*>(p);
-            ahi[0] = *reinterpret_cast<const v4i*>(p + 16);
-          } else {
-            alo[0] = zero4;
-            ahi[0] = zero4;
-          }
-        } else {
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            alo[mt] = as_v4i(ab[s][mt][0]);
-            ahi[mt] = as_v4i(ab[s][mt][1]);
-          }
+      v4i alo[MT], ahi[MT];
+      if constexpr (QM == kQLds) {
+        // Rows past M and stages past the split read clamped LDS addresses:
+        // their weights are zero, and rows past M are never stored.
+        const int kb = min(stage_kb(i), kb_end - 1);
+        const uint8_t* p = l_body + min(r16, M - 1) * ldq + (kb - kb_begin) * 128 + g4 * 32;
+        alo[0] = *reinterpret_cast<const v4i*>(p);
+        ahi[0] = *reinterpret_cast<const v4i*>(p + 16);
+      } else {
+  #pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          alo[mt] = as_v4i(ab[s][mt][0]);
+          ahi[mt] = as_v4i(ab[s][mt][1]);
         }
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          const v4i blo = nib_lo(wb[s][t]);
-          const v4i bhi = nib_hi(wb[s][t]);
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            if constexpr (GROUP) {
-              v4i p = mfma16(alo[mt], blo, zero4);
-              p = mfma16(ahi[mt], bhi, p);
-#pragma unroll
-              for (int r = 0; r < 4; ++r) facc[mt][t][r] = __fmaf_rn((float)p[r], sgb[s][t], facc[mt][t][r]);
-            } else {
-              acc[mt][t] = mfma16(alo[mt], blo, acc[mt][t]);
-              acc[mt][t] = mfma16(ahi[mt], bhi, acc[mt][t]);
-            }
-          }
-        }
-        if (i + D < iters) load_stage(s, i + D);
       }
+  #pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const v4i blo = nib_lo(wb[s][t]);
+        const v4i bhi = nib_hi(wb[s][t]);
+  #pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          if constexpr (GROUP) {
+            v4i p = mfma16(alo[mt], blo, zero4);
+            p = mfma16(ahi[mt], bhi, p);
+            const float sg = f16_to_f32(sgb[s][t]) * 0.0625f;
+  #pragma unroll
+            for (int r = 0; r < 4; ++r) facc[mt][t][r] = __fmaf_rn((float)p[r], sg, facc[mt][t][r]);
+          } else {
+            acc[mt][t] = mfma16(alo[mt], blo, acc[mt][t]);
+            acc[mt][t] = mfma16(ahi[mt], bhi, acc[mt][t]);
+          }
+        }
+      }
+      load_stage(s, i + D);
     }
   }
 
@@ -261,13 +316,14 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
     }
   lds_barrier();
 
-  const Emit emit{a, FUSED ? l_s : nullptr};
-  constexpr int kOut = MT * 16 * NT * 16;
-  const int tiles_here = min(NT, ntiles - nt0);
-  for (int o = tid; o < kOut; o += kThreads) {
+  const Emit emit{a};
+#pragma unroll
+  for (int q = 0; q < kOPT; ++q) {
+    const int o = tid + q * kThreads;
     const int row = o / (NT * 16), col = o % (NT * 16);
     const int mt = row >> 4, rr = row & 15, t = col >> 4, cc = col & 15;
-    if (row >= M || t >= tiles_here) continue;
+    if (o >= kOut || row >= M || t >= tiles_here) continue;
+    if constexpr (FUSED) sxp[q] = l_s[row];
     const int src = ((rr >> 2) * 16 + cc) * 4 + (rr & 3);
     const int n = (nt0 + t) * 16 + cc;
     if constexpr (GROUP) {
@@ -275,7 +331,7 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) v += __uint_as_float(red[((w * MT + mt) * NT + t) * 256 + src]);
       if (a.S == 1)
-        emit.group(row, n, v);
+        emit.group(row, n, v, sxp[q]);
       else
         static_cast<float*>(a.partial)[((size_t)split * M + row) * N + n] = v;
     } else {
@@ -283,7 +339,7 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) v += (int)red[((w * MT + mt) * NT + t) * 256 + src];
       if (a.S == 1)
-        emit.channel(row, n, v);
+        emit.channel(row, n, v, sxp[q], swp[q]);
       else
         static_cast<int*>(a.partial)[((size_t)split * M + row) * N + n] = v;
     }
@@ -300,21 +356,23 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   __syncthreads();
   if (!l_last) return;
   __threadfence();
-  for (int o = tid; o < kOut; o += kThreads) {
+#pragma unroll
+  for (int q = 0; q < kOPT; ++q) {
+    const int o = tid + q * kThreads;
     const int row = o / (NT * 16), col = o % (NT * 16);
     const int t = col >> 4, cc = col & 15;
-    if (row >= M || t >= tiles_here) continue;
+    if (o >= kOut || row >= M || t >= tiles_here) continue;
     const int n = (nt0 + t) * 16 + cc;
     if constexpr (GROUP) {
       const float* part = static_cast<const float*>(a.partial);
       float v = 0.0f;
       for (int s = 0; s < a.S; ++s) v += __builtin_nontemporal_load(part + ((size_t)s * M + row) * N + n);
-      emit.group(row, n, v);
+      emit.group(row, n, v, sxp[q]);
     } else {
       const int* part = static_cast<const int*>(a.partial);
       int v = 0;
       for (int s = 0; s < a.S; ++s) v += __builtin_nontemporal_load(part + ((size_t)s * M + row) * N + n);
-      emit.channel(row, n, v);
+      emit.channel(row, n, v, sxp[q], swp[q]);
     }
   }
   if (tid == 0) atomicExch(&a.counters[gid], 0u);
@@ -324,38 +382,39 @@ typedef void (*SmallMKernel)(const SmallMArgs);
 
 // MT * NT is capped at 12 (kMaxTilesPerWave): beyond it the accumulators
 // and in-flight operands no longer fit in 256 registers.
-template <int MT, int NT, bool GROUP, bool FUSED>
+template <int MT, int NT, bool GROUP, int QM>
 SmallMKernel instance() {
-  if constexpr (MT * NT <= kMaxTilesPerWave)
-    return smallm<MT, NT, GROUP, FUSED>;
+  if constexpr (MT * NT <= kMaxTilesPerWave && (QM != kQNone || !GROUP || NT <= kMaxGroupTiles) &&
+                (QM == kQNone || MT == 1))
+    return smallm<MT, NT, GROUP, QM>;
   else
     return nullptr;
 }
 
-template <int MT, bool GROUP, bool FUSED>
+template <int MT, bool GROUP, int QM>
 SmallMKernel pick_nt(int NT) {
   switch (NT) {
-    case 1: return instance<MT, 1, GROUP, FUSED>();
-    case 2: return instance<MT, 2, GROUP, FUSED>();
-    case 3: return instance<MT, 3, GROUP, FUSED>();
-    case 4: return instance<MT, 4, GROUP, FUSED>();
-    case 6: return instance<MT, 6, GROUP, FUSED>();
+    case 1: return instance<MT, 1, GROUP, QM>();
+    case 2: return instance<MT, 2, GROUP, QM>();
+    case 3: return instance<MT, 3, GROUP, QM>();
+    case 4: return instance<MT, 4, GROUP, QM>();
+    case 6: return instance<MT, 6, GROUP, QM>();
     default: return nullptr;
   }
 }
 
-SmallMKernel pick(const SmallMPlan& p) {
-  if (p.fused) {
-    if (p.MT != 1) return nullptr;
-    return p.group ? pick_nt<1, true, true>(p.NT) : pick_nt<1, false, true>(p.NT);
-  }
+template <bool GROUP>
+SmallMKernel pick_group(const SmallMPlan& p) {
+  if (p.qmode == kQLds) return pick_nt<1, GROUP, kQLds>(p.NT);
   switch (p.MT) {
-    case 1: return p.group ? pick_nt<1, true, false>(p.NT) : pick_nt<1, false, false>(p.NT);
-    case 2: return p.group ? pick_nt<2, true, false>(p.NT) : pick_nt<2, false, false>(p.NT);
-    case 4: return p.group ? pick_nt<4, true, false>(p.NT) : pick_nt<4, false, false>(p.NT);
+    case 1: return pick_nt<1, GROUP, kQNone>(p.NT);
+    case 2: return pick_nt<2, GROUP, kQNone>(p.NT);
+    case 4: return pick_nt<4, GROUP, kQNone>(p.NT);
     default: return nullptr;
   }
 }
+
+SmallMKernel pick(const SmallMPlan& p) { return p.group ? pick_group<true>(p) : pick_group<false>(p); }
 
 }  // namespace
 
@@ -370,6 +429,9 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in) {
   double best = -1.0;
   for (int nt : nts) {
     if (ntiles % nt || p.MT * nt > kMaxTilesPerWave) continue;
+    // the int8-input group kernels hold at most kMaxGroupTiles tiles (the
+    // fused decision is taken below, so stay within the tighter bound)
+    if (group && nt > kMaxGroupTiles) continue;
     for (int s : ss) {
       if (s > KB) continue;
       const int kbs = (KB + s - 1) / s;
@@ -387,10 +449,20 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in) {
     }
   }
   const int kbs = (KB + p.S - 1) / p.S;
-  p.fused = bf16_in && p.MT == 1 && (K / 8) % kThreads == 0 && M * ((K / 8) / kThreads) <= kXCache &&
-            (size_t)M * (kbs * 128 + 16) <= 96 * 1024;
+  int mp = 1;
+  while (mp < M) mp *= 2;
+  p.tpr = kThreads / (mp < 16 ? mp : 16);
+  // Fused quantize only for narrow column groups: with NT >= 3 the waves'
+  // deeper weight prologue stalls them at issue while the quantize work is
+  // still ahead, and a separate quantize kernel is faster (measured on the
+  // gate+up and down verification shapes, M = 1..16).
+  p.qmode = kQNone;
+  if (bf16_in && p.MT == 1 && p.NT <= kMaxFusedTiles && (K / 8) % p.tpr == 0 &&
+      (K / 8) / p.tpr <= kXCache && (size_t)M * (kbs * 128 + 16) <= 96 * 1024)
+    p.qmode = kQLds;
+  p.fused = p.qmode != kQNone;
   const size_t red = (size_t)kWaves * p.MT * p.NT * 1024;
-  const size_t codes = p.fused ? (size_t)M * (kbs * 128 + 16) : 0;
+  const size_t codes = p.qmode == kQLds ? (size_t)M * (kbs * 128 + 16) : 0;
   p.lds_bytes = kLdsHeader + (red > codes ? red : codes);
   return p;
 }
@@ -405,8 +477,9 @@ hipError_t launch_smallm(const SmallMPlan& p, const SmallMArgs& a, hipStream_t s
 
 const char* smallm_kernel_name(const SmallMPlan& p) {
   static thread_local char buf[96];
+  static const char* modes[] = {"int8-in", "fused-quant"};
   snprintf(buf, sizeof buf, "smallm<MT=%d,NT=%d,%s,%s> S=%d groups=%d", p.MT, p.NT,
-           p.group ? "group" : "channel", p.fused ? "fused-quant" : "int8-in", p.S, p.groups);
+           p.group ? "group" : "channel", modes[p.qmode], p.S, p.groups);
   return buf;
 }
 

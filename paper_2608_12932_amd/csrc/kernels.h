@@ -29,14 +29,17 @@ struct SmallMArgs {
   unsigned* counters;    // [groups] arrival counters (S > 1)
   int M, N, K, KB;
   int S, kbs;            // K splits and 128-k blocks per split
+  int tpr;               // fused quantize: threads per token row
   int out_kind;
 };
 struct SmallMPlan {
   int MT, NT;            // 16-row tiles, 16-column tiles per workgroup
   int S;                 // K splits over workgroups
   bool fused;            // quantize inside the GEMM
+  int qmode;             // 0 int8 codes in, 1 fused via LDS, 2 fused in registers
   bool group;            // group-wise scales
   int groups;            // workgroups along N
+  int tpr;               // fused quantize: threads per token row
   size_t lds_bytes;
 };
 SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in);

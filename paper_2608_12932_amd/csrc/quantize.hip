@@ -22,14 +22,17 @@ __global__ __launch_bounds__(kThreads) void quantize_rows(const uint16_t* __rest
   uint2* qr = reinterpret_cast<uint2*>(q + (size_t)row * K);
   const int nchunk = K / 8;
 
+  // Chunks past the row read as zeros from the buffer resource (no branch).
+  const __amdgpu_buffer_rsrc_t xres = make_rsrc(xr, (uint32_t)(K * 2));
   uint4 cache[kCache];
   uint32_t m = 0;
 #pragma unroll
   for (int j = 0; j < kCache; ++j) {
     const int c = tid + j * kThreads;
-    cache[j] = c < nchunk ? xr[c] : make_uint4(0, 0, 0, 0);
-    m = absmax_chunk(m, cache[j]);
+    cache[j] = buf_load16(xres, c < nchunk ? (uint32_t)(c * 16) : kOOB);
   }
+#pragma unroll
+  for (int j = 0; j < kCache; ++j) m = absmax_chunk(m, cache[j]);
   for (int c = tid + kCache * kThreads; c < nchunk; c += kThreads) m = absmax_chunk(m, xr[c]);
 
   __shared__ uint32_t red[kThreads / 64];

@@ -43,8 +43,12 @@ def test_packed_weight_bytes(N, K, want):
 
 
 def test_workspace_bytes_plans():
-    # gate+up verify: fused quantize, no split -> no workspace
-    assert w.w4a8_linear_workspace_bytes(16, 24576, 4096) == 0
+    # gate+up verify: codes from the quantize kernel live in the workspace
+    assert w.w4a8_linear_workspace_bytes(16, 24576, 4096) >= 16 * 4096 + 16 * 4
+    assert w.w4a8_linear_workspace_bytes(16, 24576, 4096, in_kind=w.IN_I8) == 0
+    # down verify at M=1: quantize fused into the GEMM, no split -> none
+    assert w.w4a8_linear_workspace_bytes(1, 4096, 12288) == 0
+    assert "fused-quant" in w.w4a8_linear_describe(1, 4096, 12288)
     # large M with bf16 input: codes + scales in the workspace
     ws = w.w4a8_linear_workspace_bytes(1024, 6144, 4096)
     assert ws >= 1024 * 4096 + 1024 * 4

@@ -228,6 +228,49 @@ __device__ __forceinline__ uint16_t buf_load2s(__amdgpu_buffer_rsrc_t r, uint32_
   return (uint16_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, (int)soff, kAux);
 }
 
+// ---- direct HBM -> LDS loads (LDS DMA)
+// A raw buffer descriptor as four words (base, base_hi, bytes, format) for
+// inline assembly; same range semantics as make_rsrc.
+__device__ __forceinline__ u32x4 make_rsrc_words(const void* base, uint32_t bytes) {
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  u32x4 r;
+  r[0] = (uint32_t)b;
+  r[1] = (uint32_t)(b >> 32) & 0xFFFFu;  // stride 0
+  r[2] = bytes;
+  r[3] = 0x00020000u;
+  return r;
+}
+// Each lane's 16 (or 4) bytes land at lds_addr + lane * 16 (or 4); the
+// wave's instruction fills 1 KiB (256 B) of LDS contiguously.  Issued as
+// assembly on purpose: the compiler, unable to tell which LDS stage such a
+// load fills, would otherwise wait for every one of them before any LDS
+// read and empty the prefetch ring.  Callers wait with s_waitcnt vmcnt.
+__device__ __forceinline__ void lds_dma16(u32x4 rsrc, uint32_t lds_addr, uint32_t voff, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+               : "memory");
+}
+__device__ __forceinline__ void lds_dma16_nt(u32x4 rsrc, uint32_t lds_addr, uint32_t voff, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen nt lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+               : "memory");
+}
+__device__ __forceinline__ void lds_dma4(u32x4 rsrc, uint32_t lds_addr, uint32_t voff, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+               : "memory");
+}
+// s_waitcnt constraining only the vector-memory count (gfx9 encoding:
+// vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+}
+
 template <int kAux = kCacheDefault>
 __device__ __forceinline__ uint16_t buf_load2(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return (uint16_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, kAux);

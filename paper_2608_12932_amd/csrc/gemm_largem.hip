@@ -6,12 +6,16 @@
 //   - a BM x BN output tile per workgroup, 128 k per step (one scale group);
 //     tile sizes are picked on the host so that the tile count fills the 256
 //     CUs in whole waves;
-//   - each step's int8 activation tile and packed int4 weight tile are
-//     loaded into registers one step ahead and written into the other half
-//     of a double-buffered LDS stage (one barrier per step);
-//   - activation rows are XOR-swizzled in LDS (16-byte chunk c of row r at
-//     c ^ (r & 7)) so the 32 row reads of an MFMA operand hit distinct banks;
-//     weight chunks keep the packed order, which is already conflict free;
+//   - each step's int8 activation tile and packed int4 weight tile travel
+//     from HBM straight into one stage of an R-deep LDS ring
+//     (buffer_load_dwordx4 ... lds: no registers, no VALU); step kb + R - 1
+//     is issued right after the barrier of step kb, into the stage step
+//     kb - 1 just released, so R - 1 steps of MFMA work cover the latency;
+//   - every load instruction writes 1 KiB of LDS contiguously; activation
+//     rows still land XOR-swizzled (16-byte chunk c of row r at c ^ (r & 7),
+//     so the 32 row reads of an MFMA operand hit distinct banks) because each
+//     lane fetches the global chunk that belongs at its LDS position; weight
+//     chunks keep the packed order, which is already conflict free;
 //   - every wave holds a (32 WM) x (32 WN) accumulator tile of
 //     v_mfma_i32_32x32x32_i8 blocks; the weight nibbles are unpacked in
 //     registers right before the MFMAs;
@@ -30,15 +34,23 @@ namespace w4a8 {
 
 namespace {
 
+constexpr int kRing = 4;  // LDS stages in flight
+
 template <int WM, int WN, int GM, int GN, bool GROUP>
 __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   constexpr int kThreads = GM * GN * 64;
+  constexpr int kWaves = GM * GN;
   constexpr int BM = 32 * WM * GM, BN = 32 * WN * GN;
   constexpr int kABytes = BM * 128, kBBytes = BN / 16 * kBlockBytes;
-  constexpr int kStage = kABytes + kBBytes;
-  constexpr int kACh = kABytes / 16 / kThreads, kBCh = kBBytes / 16 / kThreads;
+  constexpr int kSBytes = GROUP ? kWaves * 256 : 0;  // group scales: 256 B per wave
+  constexpr int kStage = kABytes + kBBytes + kSBytes;
+  constexpr int kACh = kABytes / 16 / kThreads, kBCh = kBBytes / 16 / kThreads;  // loads per thread per stage
   static_assert(kACh * kThreads * 16 == kABytes, "A tile must split evenly over the threads");
   static_assert(kBCh * kThreads * 16 == kBBytes, "B tile must split evenly over the threads");
+  constexpr int kSPerWave = BN / kWaves;                 // group scales each wave fetches
+  static_assert(!GROUP || (kSPerWave * kWaves == BN && kSPerWave % 2 == 0 && kSPerWave <= 128),
+                "group scales must split evenly, two per lane");
+  constexpr int kPerStage = kACh + kBCh + (GROUP ? 1 : 0);  // vector-memory instructions per stage
   extern __shared__ __align__(16) uint8_t lds[];
 
   int bid = blockIdx.x;
@@ -46,54 +58,55 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   if (a.xcd_remap) bid = (bid & 7) * (total >> 3) + (bid >> 3);
   const int tm = bid % a.tiles_m, tn = bid / a.tiles_m;
   const int m0 = tm * BM, n0 = tn * BN, nt0 = n0 / 16;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % GM, wn = wave / GM;
   const int M = a.M, N = a.N, K = a.K, KB = a.KB;
   const int ntiles = N / 16;
   const int l32 = lane & 31, g2 = lane >> 5;
 
-  // Per-tile buffer resources: rows past M and tiles past N lie outside
+  // Per-tile buffer descriptors: rows past M and tiles past N lie outside
   // them and read as zeros (no branch, no traffic).
   const int rows_here = min(BM, M - m0);
   const int tiles_here = min(BN / 16, ntiles - nt0);
-  const __amdgpu_buffer_rsrc_t ares = make_rsrc(a.xq + (size_t)m0 * K, (uint32_t)(rows_here * K));
-  const __amdgpu_buffer_rsrc_t bres =
-      make_rsrc(a.wp + (size_t)nt0 * KB * kBlockBytes, (uint32_t)(tiles_here * KB * kBlockBytes));
   const int cols_here = min(BN, N - n0);
-  const __amdgpu_buffer_rsrc_t sres =
-      make_rsrc(static_cast<const uint16_t*>(a.w_scale) + n0, (uint32_t)(((size_t)KB * N - n0) * 2));
+  const u32x4 ares = make_rsrc_words(a.xq + (size_t)m0 * K, (uint32_t)(rows_here * K));
+  const u32x4 bres = make_rsrc_words(a.wp + (size_t)nt0 * KB * kBlockBytes, (uint32_t)(tiles_here * KB * kBlockBytes));
+  const u32x4 sres = make_rsrc_words(static_cast<const uint16_t*>(a.w_scale) + n0,
+                                     GROUP ? (uint32_t)(((size_t)KB * N - n0) * 2) : 0u);
+  const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
 
-  uint4 ra[kACh], rb[kBCh];
-  // kb == KB (the prefetch after the last step) loads nothing.
-  auto gload = [&](int kb) {
+  // Load j of this thread for the A part covers LDS chunk p = j * threads +
+  // tid of the stage, i.e. row p / 8, physical chunk p % 8, which holds the
+  // logical chunk (p % 8) ^ (row % 8).  Each wave instruction fills 1 KiB.
+  uint32_t a_voff[kACh];
+#pragma unroll
+  for (int j = 0; j < kACh; ++j) {
+    const int p = j * kThreads + tid;
+    const int row = p >> 3, ch = (p & 7) ^ (row & 7);
+    a_voff[j] = (uint32_t)(row * K + ch * 16);
+  }
+  // group scales: wave w fetches columns [w kSPerWave, +kSPerWave), two per
+  // lane (4 bytes); lanes past that and columns past N read zeros
+  const int scol = wave * kSPerWave + 2 * lane;
+  const uint32_t s_voff = GROUP && 2 * lane < kSPerWave && scol < cols_here ? (uint32_t)(scol * 2) : kOOB;
+
+  // Issue step kb into its stage; past the end the loads read zeros
+  // without traffic, so every stage is the same kPerStage instructions.
+  auto issue = [&](int kb) {
     const bool ok = kb < KB;
+    const uint32_t st = lds_base + (uint32_t)((kb % kRing) * kStage);
 #pragma unroll
-    for (int i = 0; i < kACh; ++i) {
-      const int idx = tid + i * kThreads;
-      const int row = idx >> 3, ch = idx & 7;
-      ra[i] = buf_load16(ares, ok ? (uint32_t)(row * K + kb * 128 + ch * 16) : kOOB);
-    }
+    for (int j = 0; j < kACh; ++j)
+      lds_dma16(ares, st + (j * kWaves + wave) * 1024, ok ? a_voff[j] : kOOB, ok ? kb * 128 : 0);
 #pragma unroll
-    for (int i = 0; i < kBCh; ++i) {
-      const int idx = tid + i * kThreads;
-      const int blk = idx >> 6, j = idx & 63;
-      rb[i] = buf_load16<kCacheStream>(bres, ok ? (uint32_t)((blk * KB + kb) * kBlockBytes + j * 16) : kOOB);
+    for (int j = 0; j < kBCh; ++j) {
+      const int blk = j * kWaves + wave;
+      lds_dma16_nt(bres, st + kABytes + blk * 1024, ok ? (uint32_t)(lane * 16 + blk * KB * kBlockBytes) : kOOB,
+                   ok ? kb * kBlockBytes : 0);
     }
-  };
-  auto swrite = [&](int buf) {
-    uint8_t* As = lds + buf * kStage;
-    uint8_t* Bs = As + kABytes;
-#pragma unroll
-    for (int i = 0; i < kACh; ++i) {
-      const int idx = tid + i * kThreads;
-      const int row = idx >> 3, ch = idx & 7;
-      *reinterpret_cast<uint4*>(As + row * 128 + ((ch ^ (row & 7)) << 4)) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < kBCh; ++i) {
-      const int idx = tid + i * kThreads;
-      *reinterpret_cast<uint4*>(Bs + idx * 16) = rb[i];
-    }
+    if constexpr (GROUP)
+      lds_dma4(sres, st + kABytes + kBBytes + wave * 256, ok ? s_voff : kOOB, ok ? (uint32_t)((size_t)kb * N * 2) : 0u);
   };
 
   v16i acc[WM][WN];
@@ -109,19 +122,20 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
         for (int r = 0; r < 16; ++r) facc[i][j][r] = 0.0f;
     }
 
-  gload(0);
-  swrite(0);
-  __syncthreads();
-  for (int kb = 0; kb < KB; ++kb) {
-    const int buf = kb & 1;
-    gload(kb + 1);
-    uint16_t sgr[GROUP ? WN : 1];
-    if constexpr (GROUP) {
 #pragma unroll
-      for (int j = 0; j < WN; ++j) {
-        const int col = wn * 32 * WN + j * 32 + l32;
-        sgr[j] = buf_load2(sres, col < cols_here ? (uint32_t)(((size_t)kb * N + col) * 2) : kOOB);
-      }
+  for (int s = 0; s < kRing - 1; ++s) issue(s);
+
+  for (int kb = 0; kb < KB; ++kb) {
+    // This wave's loads of step kb are done once at most the kRing - 2
+    // younger stages are outstanding; the barrier then makes every wave's
+    // loads of the stage visible and proves every wave is done with the
+    // stage of step kb - 1, which the issue right after it refills.
+    wait_vmcnt<(kRing - 2) * kPerStage>();
+    lds_barrier();
+    issue(kb + kRing - 1);
+    const uint8_t* As = lds + (kb % kRing) * kStage;
+    const uint8_t* Bs = As + kABytes;
+    if constexpr (GROUP) {
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
@@ -129,8 +143,6 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
     }
-    const uint8_t* As = lds + buf * kStage;
-    const uint8_t* Bs = As + kABytes;
 #pragma unroll
     for (int tp = 0; tp < 2; ++tp) {
       const int g = tp * 2 + g2;
@@ -158,17 +170,19 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
         }
     }
     if constexpr (GROUP) {
+      const uint8_t* Ss = Bs + kBBytes;
 #pragma unroll
-      for (int i = 0; i < WM; ++i)
+      for (int j = 0; j < WN; ++j) {
+        const int col = wn * 32 * WN + j * 32 + l32;
+        const float sg = f16_to_f32(*reinterpret_cast<const uint16_t*>(Ss + (col / kSPerWave) * 256 + (col % kSPerWave) * 2)) * 0.0625f;
 #pragma unroll
-        for (int j = 0; j < WN; ++j)
+        for (int i = 0; i < WM; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            facc[i][j][r] = __fmaf_rn((float)acc[i][j][r], f16_to_f32(sgr[j]) * 0.0625f, facc[i][j][r]);
+          for (int r = 0; r < 16; ++r) facc[i][j][r] = __fmaf_rn((float)acc[i][j][r], sg, facc[i][j][r]);
+      }
     }
-    swrite(buf ^ 1);  // after the last step this fills the idle half with zeros
-    __syncthreads();
   }
+  wait_vmcnt<0>();  // the stages issued past the end
 
   // ---- epilogue: lane holds column l32, rows 8 (r / 4) + 4 g2 + r % 4
   const bool scaled = a.out_kind != kOutI32;
@@ -264,7 +278,8 @@ LargeMPlan plan_largem(int M, int N, int K, bool group) {
       p.tiles_n = tn;
     }
   }
-  p.lds_bytes = 2 * ((size_t)p.BM * 128 + (size_t)p.BN / 16 * kBlockBytes);
+  p.lds_bytes = kRing * ((size_t)p.BM * 128 + (size_t)p.BN / 16 * kBlockBytes +
+                          (group ? (size_t)p.threads / 64 * 256 : 0));
   return p;
 }
 

@@ -26,6 +26,7 @@
 // each step's int32 partial is rescaled by its fp16 group scale into an
 // fp32 accumulator).
 #include <cstdio>
+#include <type_traits>
 
 #include "device.h"
 #include "kernels.h"
@@ -109,82 +110,149 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
       lds_dma4(sres, st + kABytes + kBBytes + wave * 256, ok ? s_voff : kOOB, ok ? (uint32_t)((size_t)kb * N * 2) : 0u);
   };
 
-  v16i acc[WM][WN];
-  float facc[GROUP ? WM : 1][GROUP ? WN : 1][16];
+  // LDS read offsets of this lane's MFMA operands: activation row
+  // wm 32 WM + 32 i + l32 (its chunks c sit at c ^ (row & 7)), weight column
+  // wn 32 WN + 32 j + l32 of the stage's weight tiles.
+  const int swz = l32 & 7;
+  uint32_t a_rd[WM], b_rd[WN];
 #pragma unroll
-  for (int i = 0; i < WM; ++i)
+  for (int i = 0; i < WM; ++i) a_rd[i] = (uint32_t)((wm * 32 * WM + i * 32 + l32) * 128);
 #pragma unroll
-    for (int j = 0; j < WN; ++j) {
+  for (int j = 0; j < WN; ++j) {
+    const int col = wn * 32 * WN + j * 32 + l32;
+    b_rd[j] = (uint32_t)(kABytes + (col >> 4) * kBlockBytes + (col & 15) * 16);
+  }
+  // MFMA k half tp covers the 64 k of chunk group g = 2 tp + g2.
+  uint32_t a_ch[4];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
-      if constexpr (GROUP)
+  for (int tp = 0; tp < 2; ++tp) {
+    const int g = 2 * tp + g2;
+    a_ch[2 * tp] = (uint32_t)(((2 * g) ^ swz) << 4);
+    a_ch[2 * tp + 1] = (uint32_t)(((2 * g + 1) ^ swz) << 4);
+  }
+  uint32_t s_rd[GROUP ? WN : 1];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) facc[i][j][r] = 0.0f;
-    }
+  for (int j = 0; j < (GROUP ? WN : 1); ++j) {
+    const int col = wn * 32 * WN + j * 32 + l32;
+    s_rd[j] = (uint32_t)(kABytes + kBBytes + (col / kSPerWave) * 256 + (col % kSPerWave) * 2);
+  }
 
-#pragma unroll
-  for (int s = 0; s < kRing - 1; ++s) issue(s);
-
-  for (int kb = 0; kb < KB; ++kb) {
-    // This wave's loads of step kb are done once at most the kRing - 2
-    // younger stages are outstanding; the barrier then makes every wave's
-    // loads of the stage visible and proves every wave is done with the
-    // stage of step kb - 1, which the issue right after it refills.
-    wait_vmcnt<(kRing - 2) * kPerStage>();
-    lds_barrier();
-    issue(kb + kRing - 1);
-    const uint8_t* As = lds + (kb % kRing) * kStage;
-    const uint8_t* Bs = As + kABytes;
-    if constexpr (GROUP) {
-#pragma unroll
-      for (int i = 0; i < WM; ++i)
-#pragma unroll
-        for (int j = 0; j < WN; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
-    }
+  // One step's MFMA operands, held in registers so that the LDS reads of
+  // step kb + 1 overlap the MFMAs of step kb.
+  struct Ops {
+    v4i a[WM][4];    // activation chunks of both k halves
+    uint4 b[WN][2];  // packed weight chunk of both k halves
+    float sg[GROUP ? WN : 1];
+  };
+  auto read_ops = [&](int kb, Ops& o) {
+    const uint8_t* st = lds + (kb % kRing) * kStage;
 #pragma unroll
     for (int tp = 0; tp < 2; ++tp) {
-      const int g = tp * 2 + g2;
-      v4i alo[WM], ahi[WM], blo[WN], bhi[WN];
 #pragma unroll
       for (int i = 0; i < WM; ++i) {
-        const int row = wm * 32 * WM + i * 32 + l32;
-        const uint8_t* rp = As + row * 128;
-        alo[i] = *reinterpret_cast<const v4i*>(rp + (((2 * g) ^ (row & 7)) << 4));
-        ahi[i] = *reinterpret_cast<const v4i*>(rp + (((2 * g + 1) ^ (row & 7)) << 4));
+        o.a[i][2 * tp] = *reinterpret_cast<const v4i*>(st + a_rd[i] + a_ch[2 * tp]);
+        o.a[i][2 * tp + 1] = *reinterpret_cast<const v4i*>(st + a_rd[i] + a_ch[2 * tp + 1]);
       }
 #pragma unroll
-      for (int j = 0; j < WN; ++j) {
-        const int col = wn * 32 * WN + j * 32 + l32;
-        const uint4 w = *reinterpret_cast<const uint4*>(Bs + (col >> 4) * kBlockBytes + (g * 16 + (col & 15)) * 16);
-        blo[j] = nib_lo(w);
-        bhi[j] = nib_hi(w);
-      }
-#pragma unroll
-      for (int i = 0; i < WM; ++i)
-#pragma unroll
-        for (int j = 0; j < WN; ++j) {
-          acc[i][j] = mfma32(alo[i], blo[j], acc[i][j]);
-          acc[i][j] = mfma32(ahi[i], bhi[j], acc[i][j]);
-        }
+      for (int j = 0; j < WN; ++j)
+        o.b[j][tp] = *reinterpret_cast<const uint4*>(st + b_rd[j] + (2 * tp + g2) * 256);
     }
-    if constexpr (GROUP) {
-      const uint8_t* Ss = Bs + kBBytes;
+    if constexpr (GROUP)
 #pragma unroll
-      for (int j = 0; j < WN; ++j) {
-        const int col = wn * 32 * WN + j * 32 + l32;
-        const float sg = f16_to_f32(*reinterpret_cast<const uint16_t*>(Ss + (col / kSPerWave) * 256 + (col % kSPerWave) * 2)) * 0.0625f;
+      for (int j = 0; j < WN; ++j)
+        o.sg[j] = f16_to_f32(*reinterpret_cast<const uint16_t*>(st + s_rd[j])) * 0.0625f;
+  };
+
+  // Channel mode accumulates every step into acc[0].  Group mode rescales
+  // each step's int32 partial into facc; steps alternate between the two
+  // accumulator sets so that the rescale of one overlaps the MFMAs of the
+  // next.
+  v16i acc[GROUP ? 2 : 1][WM][WN];
+  float facc[GROUP ? WM : 1][GROUP ? WN : 1][16];
+#pragma unroll
+  for (int h = 0; h < (GROUP ? 2 : 1); ++h)
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[h][i][j][r] = 0;
+  if constexpr (GROUP)
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) facc[i][j][r] = 0.0f;
+
+  auto mma_half = [&](const Ops& o, int tp, v16i (&c)[WM][WN]) {
+    v4i blo[WN], bhi[WN];
+#pragma unroll
+    for (int j = 0; j < WN; ++j) {
+      blo[j] = nib_lo(o.b[j][tp]);
+      bhi[j] = nib_hi(o.b[j][tp]);
+    }
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j) c[i][j] = mfma32(o.a[i][2 * tp], blo[j], c[i][j]);
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j) c[i][j] = mfma32(o.a[i][2 * tp + 1], bhi[j], c[i][j]);
+  };
+
+  // Step kb: wait for stage kb + 1 (this wave's loads: at most kRing - 2
+  // younger stages outstanding); barrier: every wave's loads of stage kb + 1
+  // are visible, and every wave has finished reading step kb's operands out
+  // of stage kb (the fence waits for its LDS reads); refill stage kb with
+  // step kb + kRing; then step kb's MFMAs run from registers while step
+  // kb + 1's operands are read, one LDS read between MFMAs.  Past the last
+  // step the reads fetch values that are never used.
+  constexpr int kReads = 2 * (2 * WM + WN);  // LDS reads per step
+  constexpr int kMfma = 4 * WM * WN;         // MFMAs per step
+  auto step = [&](int kb, const Ops& cur, Ops& nxt, v16i (&c)[WM][WN]) {
+    wait_vmcnt<(kRing - 2) * kPerStage>();
+    lds_barrier();
+    issue(kb + kRing);
+    read_ops(kb + 1, nxt);
+    mma_half(cur, 0, c);
+    mma_half(cur, 1, c);
+#pragma unroll
+    for (int q = 0; q < kReads; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x0100, 1, 0);  // one LDS read
+      __builtin_amdgcn_sched_group_barrier(0x0008, 1, 0);  // one MFMA
+    }
+    __builtin_amdgcn_sched_group_barrier(0x0008, kMfma - kReads, 0);
+    if constexpr (GROUP) {
+#pragma unroll
+      for (int j = 0; j < WN; ++j)
 #pragma unroll
         for (int i = 0; i < WM; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) facc[i][j][r] = __fmaf_rn((float)acc[i][j][r], sg, facc[i][j][r]);
-      }
+          for (int r = 0; r < 16; ++r) {
+            facc[i][j][r] = __fmaf_rn((float)c[i][j][r], cur.sg[j], facc[i][j][r]);
+            c[i][j][r] = 0;
+          }
     }
-  }
-  wait_vmcnt<0>();  // the stages issued past the end
+  };
 
-  // ---- epilogue: lane holds column l32, rows 8 (r / 4) + 4 g2 + r % 4
+#pragma unroll
+  for (int s = 0; s < kRing; ++s) issue(s);
+  Ops o0, o1;
+  wait_vmcnt<(kRing - 1) * kPerStage>();
+  lds_barrier();
+  read_ops(0, o0);
+  for (int kb = 0; kb < KB; kb += 2) {
+    step(kb, o0, o1, acc[0]);
+    if (kb + 1 < KB) step(kb + 1, o1, o0, acc[GROUP ? 1 : 0]);
+  }
+
+  // ---- epilogue.  Lane holds column l32 and rows 8 q + 4 g2 + e (r = 4 q + e)
+  // of each 32 x 32 block.  The scales are fetched first (four consecutive
+  // rows' token scales in one 16-byte load), the scaled tile is staged in
+  // the LDS ring, which is free once every wave's loads have landed, and
+  // leaves as 16-byte row chunks, so every store writes whole cache lines.
   const bool scaled = a.out_kind != kOutI32;
   const __amdgpu_buffer_rsrc_t xsres = make_rsrc(a.x_scale + m0, scaled ? (uint32_t)(rows_here * 4) : 0u);
   const __amdgpu_buffer_rsrc_t wsres =
@@ -193,38 +261,64 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
   for (int j = 0; j < WN; ++j)
     swv[j] = __uint_as_float(buf_load4(wsres, (uint32_t)((wn * 32 * WN + j * 32 + l32) * 4)));
+  uint4 sx4[WM][4];
 #pragma unroll
-  for (int i = 0; i < WM; ++i) {
-    float sxv[16];
+  for (int i = 0; i < WM; ++i)
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      sxv[r] = __uint_as_float(buf_load4(xsres, (uint32_t)((wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3)) * 4)));
+    for (int q = 0; q < 4; ++q) sx4[i][q] = buf_load16(xsres, (uint32_t)((wm * 32 * WM + i * 32 + 8 * q + 4 * g2) * 4));
+  wait_vmcnt<0>();  // also the stages issued past the end
+  lds_barrier();
+
+  auto store_tile = [&](auto es_tag) {
+    constexpr int es = decltype(es_tag)::value;  // output element bytes
+    constexpr int kPitch = BN * es + 16;         // padded row: the two row halves of a store hit distinct banks
+    static_assert(BM * kPitch <= kRing * kStage, "output tile must fit the LDS ring");
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = m0 + wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3);
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
-      for (int j = 0; j < WN; ++j) {
-        const int col = n0 + wn * 32 * WN + j * 32 + l32;
-        if (row >= M || col >= N) continue;
-        const size_t o = (size_t)row * N + col;
-        float y32;
-        if constexpr (GROUP) {
-          y32 = __fmul_rn(facc[i][j][r], sxv[r]);
-        } else {
-          const int v = acc[i][j][r] >> 4;
-          if (!scaled) {
-            static_cast<int*>(a.y)[o] = v;
-            continue;
+      for (int j = 0; j < WN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3);
+          const int col = wn * 32 * WN + j * 32 + l32;
+          uint8_t* dst = lds + row * kPitch + col * es;
+          const uint4 s4 = sx4[i][r >> 2];
+          const float sx = __uint_as_float((r & 3) == 0 ? s4.x : (r & 3) == 1 ? s4.y : (r & 3) == 2 ? s4.z : s4.w);
+          float y32;
+          if constexpr (GROUP) {
+            y32 = __fmul_rn(facc[i][j][r], sx);
+          } else {
+            const int v = acc[0][i][j][r] >> 4;
+            if (a.out_kind == kOutI32) {
+              *reinterpret_cast<int*>(dst) = v;
+              continue;
+            }
+            y32 = __fmul_rn(__fmul_rn((float)v, sx), swv[j]);
           }
-          y32 = __fmul_rn(__fmul_rn((float)v, sxv[r]), swv[j]);
+          if constexpr (es == 4)
+            *reinterpret_cast<float*>(dst) = y32;
+          else
+            *reinterpret_cast<uint16_t*>(dst) = (uint16_t)f32_to_bf16(y32);
         }
-        if (a.out_kind == kOutF32)
-          static_cast<float*>(a.y)[o] = y32;
-        else
-          static_cast<uint16_t*>(a.y)[o] = (uint16_t)f32_to_bf16(y32);
-      }
+    lds_barrier();
+    constexpr int kRowChunks = BN * es / 16;
+    constexpr int kChunks = BM * kRowChunks;
+    static_assert(kChunks % kThreads == 0, "output chunks must split evenly over the threads");
+#pragma unroll
+    for (int it = 0; it < kChunks / kThreads; ++it) {
+      const int p = it * kThreads + tid;
+      const int row = p / kRowChunks, c = p % kRowChunks;
+      const uint4 v = *reinterpret_cast<const uint4*>(lds + row * kPitch + c * 16);
+      // N is a multiple of 16 and a chunk holds 4 or 8 columns, so a chunk
+      // is either wholly inside the output or wholly past its last column
+      if (row < rows_here && c * (16 / es) < cols_here)
+        *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.y) + ((size_t)(m0 + row) * N + n0) * es + c * 16) = v;
     }
-  }
+  };
+  if (a.out_kind == kOutBF16)
+    store_tile(std::integral_constant<int, 2>{});
+  else
+    store_tile(std::integral_constant<int, 4>{});
 }
 
 typedef void (*LargeMKernel)(const LargeMArgs);

@@ -204,6 +204,15 @@ constexpr uint32_t kOOB = 0x80000000u;       // offset beyond any range used her
 constexpr int kCacheDefault = 0;
 constexpr int kCacheStream = 2;              // non-temporal: read once, do not keep
 
+// A pointer the compiler may have placed in vector registers although it
+// is the same in every lane, moved to scalar registers (so that a buffer
+// descriptor built from it stays scalar).
+template <class T>
+__device__ __forceinline__ T* uniform_ptr(T* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v), hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<T*>((uintptr_t)(((uint64_t)hi << 32) | lo));
+}
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
@@ -240,6 +249,18 @@ __device__ __forceinline__ u32x4 make_rsrc_words(const void* base, uint32_t byte
   r[3] = 0x00020000u;
   return r;
 }
+// The scalar operands of the buffer-to-LDS loads are wave-uniform by
+// construction; readfirstlane keeps them in scalar registers even where
+// register pressure made the compiler hold a copy in vector registers.
+__device__ __forceinline__ u32x4 sgpr4(u32x4 r) {
+  u32x4 o;
+  o[0] = __builtin_amdgcn_readfirstlane(r[0]);
+  o[1] = __builtin_amdgcn_readfirstlane(r[1]);
+  o[2] = __builtin_amdgcn_readfirstlane(r[2]);
+  o[3] = __builtin_amdgcn_readfirstlane(r[3]);
+  return o;
+}
+__device__ __forceinline__ uint32_t sgpr1(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 // Each lane's 16 (or 4) bytes land at lds_addr + lane * 16 (or 4); the
 // wave's instruction fills 1 KiB (256 B) of LDS contiguously.  Issued as
 // assembly on purpose: the compiler, unable to tell which LDS stage such a
@@ -248,19 +269,19 @@ __device__ __forceinline__ u32x4 make_rsrc_words(const void* base, uint32_t byte
 __device__ __forceinline__ void lds_dma16(u32x4 rsrc, uint32_t lds_addr, uint32_t voff, uint32_t soff) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                :
-               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+               : "s"(sgpr1(lds_addr)), "v"(voff), "s"(sgpr4(rsrc)), "s"(sgpr1(soff))
                : "memory");
 }
 __device__ __forceinline__ void lds_dma16_nt(u32x4 rsrc, uint32_t lds_addr, uint32_t voff, uint32_t soff) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen nt lds"
                :
-               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+               : "s"(sgpr1(lds_addr)), "v"(voff), "s"(sgpr4(rsrc)), "s"(sgpr1(soff))
                : "memory");
 }
 __device__ __forceinline__ void lds_dma4(u32x4 rsrc, uint32_t lds_addr, uint32_t voff, uint32_t soff) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
                :
-               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+               : "s"(sgpr1(lds_addr)), "v"(voff), "s"(sgpr4(rsrc)), "s"(sgpr1(soff))
                : "memory");
 }
 // s_waitcnt constraining only the vector-memory count (gfx9 encoding:

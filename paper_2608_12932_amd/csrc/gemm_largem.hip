@@ -92,22 +92,25 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   const int scol = wave * kSPerWave + 2 * lane;
   const uint32_t s_voff = GROUP && 2 * lane < kSPerWave && scol < cols_here ? (uint32_t)(scol * 2) : kOOB;
 
-  // Issue step kb into its stage; past the end the loads read zeros
-  // without traffic, so every stage is the same kPerStage instructions.
-  auto issue = [&](int kb) {
+  // Vector-memory instruction d of step kb's stage fill (A loads, then B
+  // loads, then the group scales).  Past the end the loads read zeros
+  // without traffic, so every step issues the same kPerStage instructions.
+  uint32_t b_voff[kBCh];
+#pragma unroll
+  for (int j = 0; j < kBCh; ++j) b_voff[j] = (uint32_t)(lane * 16 + (j * kWaves + wave) * KB * kBlockBytes);
+  // A step past the end gets the scalar offset kOOB: every lane's offset
+  // then lies past the descriptor's range (no vector select needed).
+  auto issue_one = [&](int kb, int d) {
     const bool ok = kb < KB;
     const uint32_t st = lds_base + (uint32_t)((kb % kRing) * kStage);
-#pragma unroll
-    for (int j = 0; j < kACh; ++j)
-      lds_dma16(ares, st + (j * kWaves + wave) * 1024, ok ? a_voff[j] : kOOB, ok ? kb * 128 : 0);
-#pragma unroll
-    for (int j = 0; j < kBCh; ++j) {
-      const int blk = j * kWaves + wave;
-      lds_dma16_nt(bres, st + kABytes + blk * 1024, ok ? (uint32_t)(lane * 16 + blk * KB * kBlockBytes) : kOOB,
-                   ok ? kb * kBlockBytes : 0);
+    if (d < kACh) {
+      lds_dma16(ares, st + (d * kWaves + wave) * 1024, a_voff[d], ok ? kb * 128 : kOOB);
+    } else if (d < kACh + kBCh) {
+      const int blk = (d - kACh) * kWaves + wave;
+      lds_dma16_nt(bres, st + kABytes + blk * 1024, b_voff[d - kACh], ok ? kb * kBlockBytes : kOOB);
+    } else if constexpr (GROUP) {
+      lds_dma4(sres, st + kABytes + kBBytes + wave * 256, s_voff, ok ? (uint32_t)((size_t)kb * N * 2) : kOOB);
     }
-    if constexpr (GROUP)
-      lds_dma4(sres, st + kABytes + kBBytes + wave * 256, ok ? s_voff : kOOB, ok ? (uint32_t)((size_t)kb * N * 2) : 0u);
   };
 
   // LDS read offsets of this lane's MFMA operands: activation row
@@ -122,7 +125,8 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
     const int col = wn * 32 * WN + j * 32 + l32;
     b_rd[j] = (uint32_t)(kABytes + (col >> 4) * kBlockBytes + (col & 15) * 16);
   }
-  // MFMA k half tp covers the 64 k of chunk group g = 2 tp + g2.
+  // MFMA k half tp covers the 64 k of chunk group g = 2 tp + g2: activation
+  // chunks 2 g and 2 g + 1, weight chunk g (low nibbles, then high nibbles).
   uint32_t a_ch[4];
 #pragma unroll
   for (int tp = 0; tp < 2; ++tp) {
@@ -140,28 +144,48 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   // One step's MFMA operands, held in registers so that the LDS reads of
   // step kb + 1 overlap the MFMAs of step kb.
   struct Ops {
-    v4i a[WM][4];    // activation chunks of both k halves
-    uint4 b[WN][2];  // packed weight chunk of both k halves
+    v4i a[WM][4];             // activation chunks of both k halves
+    uint4 b[WN][2];           // packed weight chunk of both k halves
+    v4i lo0[WN], hi0[WN];     // k half 0's weight nibbles, unpacked ahead of the step
     float sg[GROUP ? WN : 1];
   };
-  auto read_ops = [&](int kb, Ops& o) {
+  constexpr int kReadsTp = 2 * WM + WN;
+  constexpr int kReads = 2 * kReadsTp + (GROUP ? WN : 0);  // LDS reads per step
+  // LDS read r of step kb's operands: per k half the weight chunks first
+  // (half 0's are unpacked while the previous step still runs), then the
+  // activation chunks; the group scales last.
+  auto read_one = [&](int kb, int r, Ops& o) {
     const uint8_t* st = lds + (kb % kRing) * kStage;
-#pragma unroll
-    for (int tp = 0; tp < 2; ++tp) {
-#pragma unroll
-      for (int i = 0; i < WM; ++i) {
-        o.a[i][2 * tp] = *reinterpret_cast<const v4i*>(st + a_rd[i] + a_ch[2 * tp]);
-        o.a[i][2 * tp + 1] = *reinterpret_cast<const v4i*>(st + a_rd[i] + a_ch[2 * tp + 1]);
-      }
-#pragma unroll
-      for (int j = 0; j < WN; ++j)
-        o.b[j][tp] = *reinterpret_cast<const uint4*>(st + b_rd[j] + (2 * tp + g2) * 256);
+    if (r < 2 * kReadsTp) {
+      const int tp = r / kReadsTp, u = r % kReadsTp;
+      if (u < WN)
+        o.b[u][tp] = *reinterpret_cast<const uint4*>(st + b_rd[u] + (2 * tp + g2) * 256);
+      else
+        o.a[(u - WN) / 2][2 * tp + ((u - WN) & 1)] =
+            *reinterpret_cast<const v4i*>(st + a_rd[(u - WN) / 2] + a_ch[2 * tp + ((u - WN) & 1)]);
+    } else if constexpr (GROUP) {
+      const int j = r - 2 * kReadsTp;
+      o.sg[j] = f16_to_f32(*reinterpret_cast<const uint16_t*>(st + s_rd[j])) * 0.0625f;
     }
-    if constexpr (GROUP)
-#pragma unroll
-      for (int j = 0; j < WN; ++j)
-        o.sg[j] = f16_to_f32(*reinterpret_cast<const uint16_t*>(st + s_rd[j])) * 0.0625f;
   };
+
+  // The epilogue's scales, fetched now so that their latency hides behind
+  // the main loop: four consecutive rows' token scales per 16-byte load
+  // (rows 8 q + 4 g2 + e of block i), one channel scale per column block.
+  const bool scaled = a.out_kind != kOutI32;
+  const __amdgpu_buffer_rsrc_t xsres =
+      make_rsrc(uniform_ptr(a.x_scale + m0), sgpr1(scaled ? (uint32_t)(rows_here * 4) : 0u));
+  const __amdgpu_buffer_rsrc_t wsres = make_rsrc(uniform_ptr(static_cast<const float*>(a.w_scale) + n0),
+                                                 sgpr1((!GROUP && scaled) ? (uint32_t)(cols_here * 4) : 0u));
+  float swv[WN];
+#pragma unroll
+  for (int j = 0; j < WN; ++j)
+    swv[j] = __uint_as_float(buf_load4(wsres, (uint32_t)((wn * 32 * WN + j * 32 + l32) * 4)));
+  uint4 sx4[WM][4];
+#pragma unroll
+  for (int i = 0; i < WM; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sx4[i][q] = buf_load16(xsres, (uint32_t)((wm * 32 * WM + i * 32 + 8 * q + 4 * g2) * 4));
 
   // Channel mode accumulates every step into acc[0].  Group mode rescales
   // each step's int32 partial into facc; steps alternate between the two
@@ -185,121 +209,171 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) facc[i][j][r] = 0.0f;
 
-  auto mma_half = [&](const Ops& o, int tp, v16i (&c)[WM][WN]) {
-    v4i blo[WN], bhi[WN];
-#pragma unroll
-    for (int j = 0; j < WN; ++j) {
-      blo[j] = nib_lo(o.b[j][tp]);
-      bhi[j] = nib_hi(o.b[j][tp]);
-    }
-#pragma unroll
-    for (int i = 0; i < WM; ++i)
-#pragma unroll
-      for (int j = 0; j < WN; ++j) c[i][j] = mfma32(o.a[i][2 * tp], blo[j], c[i][j]);
-#pragma unroll
-    for (int i = 0; i < WM; ++i)
-#pragma unroll
-      for (int j = 0; j < WN; ++j) c[i][j] = mfma32(o.a[i][2 * tp + 1], bhi[j], c[i][j]);
+  // Unpacking one 4-byte word of packed weights into its low- and
+  // high-nibble MFMA operand words.
+  // Written as assembly so that the compiler keeps each unpack in the MFMA
+  // slot it is dealt to instead of gathering them in front of their first
+  // use.
+  auto unpack_word = [](const uint4& c, int e, v4i& lo, v4i& hi) {
+    const uint32_t w = e == 0 ? c.x : e == 1 ? c.y : e == 2 ? c.z : c.w;
+    int l, h;
+    asm volatile(
+        "v_lshlrev_b32 %0, 4, %2\n\t"
+        "v_and_b32 %0, 0xf0f0f0f0, %0\n\t"
+        "v_and_b32 %1, 0xf0f0f0f0, %2"
+        : "=&v"(l), "=&v"(h)
+        : "v"(w));
+    lo[e] = l;
+    hi[e] = h;
+  };
+  auto unpack0 = [&](Ops& o, int u) {  // word u of k half 0
+    unpack_word(o.b[u / 4][0], u % 4, o.lo0[u / 4], o.hi0[u / 4]);
   };
 
   // Step kb: wait for stage kb + 1 (this wave's loads: at most kRing - 2
   // younger stages outstanding); barrier: every wave's loads of stage kb + 1
   // are visible, and every wave has finished reading step kb's operands out
-  // of stage kb (the fence waits for its LDS reads); refill stage kb with
-  // step kb + kRing; then step kb's MFMAs run from registers while step
-  // kb + 1's operands are read, one LDS read between MFMAs.  Past the last
-  // step the reads fetch values that are never used.
-  constexpr int kReads = 2 * (2 * WM + WN);  // LDS reads per step
-  constexpr int kMfma = 4 * WM * WN;         // MFMAs per step
-  auto step = [&](int kb, const Ops& cur, Ops& nxt, v16i (&c)[WM][WN]) {
+  // of stage kb (the fence waits for its LDS reads).  Then the step's MFMAs
+  // run from registers, one per slot, and every other instruction of the
+  // step is dealt out evenly over the slots so that the matrix core never
+  // waits on a burst: the refill of stage kb with step kb + kRing, the LDS
+  // reads of step kb + 1's operands, the unpacking of this step's second k
+  // half (first half of the slots) and of step kb + 1's first k half
+  // (second half of the slots), and in group mode the rescale of the
+  // previous step's partial sums.  Past the last step the reads fetch
+  // values that are never used.
+  constexpr int kMfma = 4 * WM * WN;  // MFMAs per step
+  constexpr int kHalf = kMfma / 2;
+  constexpr int kUnits = 4 * WN;      // weight words per k half
+  constexpr int kRescale = WM * WN * 16;
+  static_assert(kRescale % kMfma == 0, "rescale work must split evenly over the MFMA slots");
+  float sg_prev[GROUP ? WN : 1];
+#pragma unroll
+  for (int j = 0; j < (GROUP ? WN : 1); ++j) sg_prev[j] = 0.0f;
+  auto step = [&](int kb, const Ops& cur, Ops& nxt, v16i (&c)[WM][WN], v16i (&prev)[WM][WN]) {
     wait_vmcnt<(kRing - 2) * kPerStage>();
     lds_barrier();
-    issue(kb + kRing);
-    read_ops(kb + 1, nxt);
-    mma_half(cur, 0, c);
-    mma_half(cur, 1, c);
+    v4i lo1[WN], hi1[WN];
 #pragma unroll
-    for (int q = 0; q < kReads; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x0100, 1, 0);  // one LDS read
-      __builtin_amdgcn_sched_group_barrier(0x0008, 1, 0);  // one MFMA
+    for (int q = 0; q < kMfma; ++q) {
+      // MFMA q: k half tp, nibble half h, block (i, j)
+      const int tp = q / (2 * WM * WN), h = (q / (WM * WN)) % 2, i = (q / WN) % WM, j = q % WN;
+      const v4i& bop = tp == 0 ? (h ? cur.hi0[j] : cur.lo0[j]) : (h ? hi1[j] : lo1[j]);
+      c[i][j] = mfma32(cur.a[i][2 * tp + h], bop, c[i][j]);
+#pragma unroll
+      for (int d = 0; d < kPerStage; ++d)
+        if (d * kMfma / kPerStage == q) issue_one(kb + kRing, d);
+#pragma unroll
+      for (int r = 0; r < kReads; ++r)
+        if (r * kMfma / kReads == q) read_one(kb + 1, r, nxt);
+#pragma unroll
+      for (int u = 0; u < kUnits; ++u) {
+        if (q < kHalf && u * kHalf / kUnits == q) unpack_word(cur.b[u / 4][1], u % 4, lo1[u / 4], hi1[u / 4]);
+        if (q >= kHalf && u * kHalf / kUnits == q - kHalf) unpack0(nxt, u);
+      }
+      if constexpr (GROUP) {
+#pragma unroll
+        for (int t = 0; t < kRescale / kMfma; ++t) {
+          const int e = q * (kRescale / kMfma) + t;
+          const int ri = e / (WN * 16), rj = (e / 16) % WN, rr = e % 16;
+          facc[ri][rj][rr] = __fmaf_rn((float)prev[ri][rj][rr], sg_prev[rj], facc[ri][rj][rr]);
+          prev[ri][rj][rr] = 0;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x0008, kMfma - kReads, 0);
-    if constexpr (GROUP) {
+    if constexpr (GROUP)
 #pragma unroll
-      for (int j = 0; j < WN; ++j)
-#pragma unroll
-        for (int i = 0; i < WM; ++i)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            facc[i][j][r] = __fmaf_rn((float)c[i][j][r], cur.sg[j], facc[i][j][r]);
-            c[i][j][r] = 0;
-          }
-    }
+      for (int j = 0; j < WN; ++j) sg_prev[j] = cur.sg[j];
   };
 
 #pragma unroll
-  for (int s = 0; s < kRing; ++s) issue(s);
+  for (int st = 0; st < kRing; ++st)
+#pragma unroll
+    for (int d = 0; d < kPerStage; ++d) issue_one(st, d);
   Ops o0, o1;
-  wait_vmcnt<(kRing - 1) * kPerStage>();
+  wait_vmcnt<(kRing - 1) * kPerStage>();  // stage 0 (and the scales, issued before it)
   lds_barrier();
-  read_ops(0, o0);
+#pragma unroll
+  for (int r = 0; r < kReads; ++r) read_one(0, r, o0);
+#pragma unroll
+  for (int u = 0; u < kUnits; ++u) unpack0(o0, u);
   for (int kb = 0; kb < KB; kb += 2) {
-    step(kb, o0, o1, acc[0]);
-    if (kb + 1 < KB) step(kb + 1, o1, o0, acc[GROUP ? 1 : 0]);
+    step(kb, o0, o1, acc[0], acc[GROUP ? 1 : 0]);
+    if (kb + 1 < KB) step(kb + 1, o1, o0, acc[GROUP ? 1 : 0], acc[0]);
   }
+  if constexpr (GROUP) {
+    // the last step's partial sums (the set of step KB - 1)
+    auto rescale_last = [&](v16i (&last)[WM][WN]) {
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) facc[i][j][r] = __fmaf_rn((float)last[i][j][r], sg_prev[j], facc[i][j][r]);
+    };
+    if (KB & 1)
+      rescale_last(acc[0]);
+    else
+      rescale_last(acc[1]);
+  }
+  wait_vmcnt<0>();  // the stages issued past the end
+  lds_barrier();    // every wave is done with the ring
 
   // ---- epilogue.  Lane holds column l32 and rows 8 q + 4 g2 + e (r = 4 q + e)
-  // of each 32 x 32 block.  The scales are fetched first (four consecutive
-  // rows' token scales in one 16-byte load), the scaled tile is staged in
-  // the LDS ring, which is free once every wave's loads have landed, and
-  // leaves as 16-byte row chunks, so every store writes whole cache lines.
-  const bool scaled = a.out_kind != kOutI32;
-  const __amdgpu_buffer_rsrc_t xsres = make_rsrc(a.x_scale + m0, scaled ? (uint32_t)(rows_here * 4) : 0u);
-  const __amdgpu_buffer_rsrc_t wsres =
-      make_rsrc(static_cast<const float*>(a.w_scale) + n0, (!GROUP && scaled) ? (uint32_t)(cols_here * 4) : 0u);
-  float swv[WN];
-#pragma unroll
-  for (int j = 0; j < WN; ++j)
-    swv[j] = __uint_as_float(buf_load4(wsres, (uint32_t)((wn * 32 * WN + j * 32 + l32) * 4)));
-  uint4 sx4[WM][4];
-#pragma unroll
-  for (int i = 0; i < WM; ++i)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) sx4[i][q] = buf_load16(xsres, (uint32_t)((wm * 32 * WM + i * 32 + 8 * q + 4 * g2) * 4));
-  wait_vmcnt<0>();  // also the stages issued past the end
-  lds_barrier();
-
+  // of each 32 x 32 block.  The scaled tile is staged in the idle LDS ring
+  // and leaves as 16-byte row chunks, so every store writes whole cache
+  // lines.  bf16 results are first paired across adjacent lanes (columns
+  // 2 p and 2 p + 1; the even lane takes row r, the odd lane row r + 1) so
+  // that every LDS write is a whole dword.
+  auto result = [&](int i, int j, int r) -> float {
+    const uint4 s4 = sx4[i][r >> 2];
+    const float sx = __uint_as_float((r & 3) == 0 ? s4.x : (r & 3) == 1 ? s4.y : (r & 3) == 2 ? s4.z : s4.w);
+    if constexpr (GROUP) {
+      return __fmul_rn(facc[i][j][r], sx);
+    } else {
+      return __fmul_rn(__fmul_rn((float)(acc[0][i][j][r] >> 4), sx), swv[j]);
+    }
+  };
   auto store_tile = [&](auto es_tag) {
     constexpr int es = decltype(es_tag)::value;  // output element bytes
-    constexpr int kPitch = BN * es + 16;         // padded row: the two row halves of a store hit distinct banks
+    // Row pitch: one half-wave's writes (bf16: rows R and R + 1 of 64 bytes;
+    // 4-byte kinds: one 128-byte row) cover all 32 banks once.
+    constexpr int kPitch = es == 2 ? BN * 2 + 64 : BN * 4 + 16;
     static_assert(BM * kPitch <= kRing * kStage, "output tile must fit the LDS ring");
+    if constexpr (es == 2) {
+      const bool odd = lane & 1;
 #pragma unroll
-    for (int i = 0; i < WM; ++i)
+      for (int i = 0; i < WM; ++i)
 #pragma unroll
-      for (int j = 0; j < WN; ++j)
+        for (int j = 0; j < WN; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3);
-          const int col = wn * 32 * WN + j * 32 + l32;
-          uint8_t* dst = lds + row * kPitch + col * es;
-          const uint4 s4 = sx4[i][r >> 2];
-          const float sx = __uint_as_float((r & 3) == 0 ? s4.x : (r & 3) == 1 ? s4.y : (r & 3) == 2 ? s4.z : s4.w);
-          float y32;
-          if constexpr (GROUP) {
-            y32 = __fmul_rn(facc[i][j][r], sx);
-          } else {
-            const int v = acc[0][i][j][r] >> 4;
-            if (a.out_kind == kOutI32) {
-              *reinterpret_cast<int*>(dst) = v;
-              continue;
-            }
-            y32 = __fmul_rn(__fmul_rn((float)v, sx), swv[j]);
+          for (int rp = 0; rp < 8; ++rp) {
+            const uint32_t b0 = f32_to_bf16(result(i, j, 2 * rp)), b1 = f32_to_bf16(result(i, j, 2 * rp + 1));
+            const uint32_t recv = (uint32_t)__builtin_amdgcn_mov_dpp((int)(odd ? b0 : b1), 0xB1, 0xF, 0xF, false);
+            const uint32_t word = odd ? (recv | (b1 << 16)) : (b0 | (recv << 16));
+            const int r = 2 * rp + (odd ? 1 : 0);
+            const int row = wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3);
+            const int col = wn * 32 * WN + j * 32 + (l32 & ~1);
+            *reinterpret_cast<uint32_t*>(lds + row * kPitch + col * 2) = word;
           }
-          if constexpr (es == 4)
-            *reinterpret_cast<float*>(dst) = y32;
-          else
-            *reinterpret_cast<uint16_t*>(dst) = (uint16_t)f32_to_bf16(y32);
-        }
+    } else {
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3);
+            const int col = wn * 32 * WN + j * 32 + l32;
+            uint32_t v;
+            if constexpr (GROUP)
+              v = __float_as_uint(result(i, j, r));
+            else
+              v = a.out_kind == kOutI32 ? (uint32_t)(acc[0][i][j][r] >> 4) : __float_as_uint(result(i, j, r));
+            *reinterpret_cast<uint32_t*>(lds + row * kPitch + col * 4) = v;
+          }
+    }
     lds_barrier();
     constexpr int kRowChunks = BN * es / 16;
     constexpr int kChunks = BM * kRowChunks;
@@ -307,12 +381,12 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
     for (int it = 0; it < kChunks / kThreads; ++it) {
       const int p = it * kThreads + tid;
-      const int row = p / kRowChunks, c = p % kRowChunks;
-      const uint4 v = *reinterpret_cast<const uint4*>(lds + row * kPitch + c * 16);
+      const int row = p / kRowChunks, cc = p % kRowChunks;
+      const uint4 v = *reinterpret_cast<const uint4*>(lds + row * kPitch + cc * 16);
       // N is a multiple of 16 and a chunk holds 4 or 8 columns, so a chunk
       // is either wholly inside the output or wholly past its last column
-      if (row < rows_here && c * (16 / es) < cols_here)
-        *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.y) + ((size_t)(m0 + row) * N + n0) * es + c * 16) = v;
+      if (row < rows_here && cc * (16 / es) < cols_here)
+        *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.y) + ((size_t)(m0 + row) * N + n0) * es + cc * 16) = v;
     }
   };
   if (a.out_kind == kOutBF16)
@@ -326,20 +400,21 @@ typedef void (*LargeMKernel)(const LargeMArgs);
 struct TileCfg {
   int WM, WN, GM, GN;
   double quality;  // relative efficiency of the tile shape (operand reuse)
+  bool group_ok;   // fits the registers with group-mode accumulators
 };
 // BM = 32 WM GM, BN = 32 WN GN
 constexpr TileCfg kMenu[] = {
-    {2, 3, 2, 2, 1.00},  // 128 x 192, 4 waves
-    {2, 2, 2, 2, 0.95},  // 128 x 128, 4 waves
-    {1, 3, 2, 1, 0.85},  // 64 x 96, 2 waves
-    {1, 1, 2, 2, 0.70},  // 64 x 64, 4 waves
+    {2, 3, 2, 2, 1.00, false},  // 128 x 192, 4 waves
+    {2, 2, 2, 2, 0.95, true},   // 128 x 128, 4 waves
+    {1, 3, 2, 1, 0.85, true},   // 64 x 96, 2 waves
+    {1, 1, 2, 2, 0.70, true},   // 64 x 64, 4 waves
 };
 constexpr int kMenuSize = sizeof(kMenu) / sizeof(kMenu[0]);
 
 template <bool GROUP>
 LargeMKernel pick_cfg(int cfg) {
   switch (cfg) {
-    case 0: return largem<2, 3, 2, 2, GROUP>;
+    case 0: return GROUP ? nullptr : largem<2, 3, 2, 2, false>;
     case 1: return largem<2, 2, 2, 2, GROUP>;
     case 2: return largem<1, 3, 2, 1, GROUP>;
     case 3: return largem<1, 1, 2, 2, GROUP>;
@@ -356,6 +431,7 @@ LargeMPlan plan_largem(int M, int N, int K, bool group) {
   double best = -1.0;
   for (int c = 0; c < kMenuSize; ++c) {
     const TileCfg& t = kMenu[c];
+    if (group && !t.group_ok) continue;
     const int BM = 32 * t.WM * t.GM, BN = 32 * t.WN * t.GN;
     const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
     const long tiles = (long)tm * tn;

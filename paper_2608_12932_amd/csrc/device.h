@@ -82,6 +82,19 @@ __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
   return u >> 16;
 }
 
+// Two floats to bf16 with the hardware conversion (round to nearest even;
+// bit-identical to f32_to_bf16 for every input but NaN, whose payload it
+// keeps): low half from lo, high half from hi.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float float2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16x2_bits(float lo, float hi) {
+  const float2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+// NaN (any sign or payload) replaced by the canonical quiet NaN; other
+// values kept.
+__device__ __forceinline__ float canonical_nan(float f) { return f != f ? __uint_as_float(0x7FC00000u) : f; }
+
 __device__ __forceinline__ float f16_to_f32(uint16_t h) {
   _Float16 v;
   memcpy(&v, &h, 2);

@@ -342,16 +342,24 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
     constexpr int kPitch = es == 2 ? BN * 2 + 64 : BN * 4 + 16;
     static_assert(BM * kPitch <= kRing * kStage, "output tile must fit the LDS ring");
     if constexpr (es == 2) {
+      // NaN results become the canonical quiet NaN (sign and payload of a NaN
+      // product vary), which the hardware conversion (round to nearest even,
+      // bit-identical to f32_to_bf16 for every other input) turns into 0x7FC0.
+      // A lane converts rows r and r + 1 of its column into one word, swaps
+      // words with its neighbour and keeps the two halves of its row: the
+      // even lane bytes {own 0-1, partner 0-1}, the odd lane {partner 2-3,
+      // own 2-3}.
       const bool odd = lane & 1;
+      const uint32_t sel = odd ? 0x03020706u : 0x05040100u;
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
         for (int j = 0; j < WN; ++j)
 #pragma unroll
           for (int rp = 0; rp < 8; ++rp) {
-            const uint32_t b0 = f32_to_bf16(result(i, j, 2 * rp)), b1 = f32_to_bf16(result(i, j, 2 * rp + 1));
-            const uint32_t recv = (uint32_t)__builtin_amdgcn_mov_dpp((int)(odd ? b0 : b1), 0xB1, 0xF, 0xF, false);
-            const uint32_t word = odd ? (recv | (b1 << 16)) : (b0 | (recv << 16));
+            const uint32_t pair = bf16x2_bits(canonical_nan(result(i, j, 2 * rp)), canonical_nan(result(i, j, 2 * rp + 1)));
+            const uint32_t recv = (uint32_t)__builtin_amdgcn_mov_dpp((int)pair, 0xB1, 0xF, 0xF, false);
+            const uint32_t word = __builtin_amdgcn_perm(recv, pair, sel);
             const int r = 2 * rp + (odd ? 1 : 0);
             const int row = wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3);
             const int col = wn * 32 * WN + j * 32 + (l32 & ~1);

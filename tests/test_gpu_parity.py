@@ -206,3 +206,33 @@ def test_minimum_and_extreme_shapes():
         assert (acc[0] == -1016 * K).all()
         if M > 1:
             assert (acc[1] == 1016 * K).all()
+
+
+def test_nan_and_inf_scales():
+    # Non-finite scales propagate as in the reference arithmetic: inf x 0 and
+    # NaN inputs give NaN, which the bf16 output writes as 0x7FC0 whatever
+    # the input NaN's payload; +-inf scales give +-inf or NaN.
+    for M in (8, 300):
+        K, N = 256, 96
+        x = I.activations(M, K, 901)
+        W, s = I.weights(N, K, 902)
+        W = W.copy()
+        W[5] = 0  # an all-zero channel under an infinite scale: inf x 0
+        s = s.copy()
+        s_bits = s.view(np.uint32)
+        s_bits[3] = 0x7FA12345   # signalling NaN with a payload
+        s_bits[7] = 0xFFC00001   # negative quiet NaN with a payload
+        s[5] = np.inf
+        s[11] = -np.inf
+        s[13] = 0.0
+        q, sx = oracle.quantize_act(x)
+        sx = sx.copy()
+        sx.view(np.uint32)[2] = 0x7FC0BEEF
+        sx[4] = np.inf
+        ref = oracle.linear_q(q, sx, W, s_w=s, nthreads=NTHREADS)
+        wp = pack(W)
+        yb = run_linear(x, wp, s, N, group=False, out_kind=w.OUT_BF16, codes=(q, sx))
+        np.testing.assert_array_equal(yb, ref["y"], err_msg=f"M={M}: bf16 with non-finite scales")
+        y32 = run_linear(x, wp, s, N, group=False, out_kind=w.OUT_F32, codes=(q, sx))
+        np.testing.assert_array_equal(y32, ref["y32"], err_msg=f"M={M}: fp32 with non-finite scales")
+        assert np.isnan(y32[:, 3]).all() and np.isnan(y32[2]).all() and np.isnan(y32[:, 5]).all()

@@ -226,6 +226,8 @@ __device__ __forceinline__ T* uniform_ptr(T* p) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v), hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
   return reinterpret_cast<T*>((uintptr_t)(((uint64_t)hi << 32) | lo));
 }
+// The same for a 32-bit value.
+__device__ __forceinline__ uint32_t uniform_u32(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
@@ -262,39 +264,30 @@ __device__ __forceinline__ u32x4 make_rsrc_words(const void* base, uint32_t byte
   r[3] = 0x00020000u;
   return r;
 }
-// The scalar operands of the buffer-to-LDS loads are wave-uniform by
-// construction; readfirstlane keeps them in scalar registers even where
-// register pressure made the compiler hold a copy in vector registers.
-__device__ __forceinline__ u32x4 sgpr4(u32x4 r) {
-  u32x4 o;
-  o[0] = __builtin_amdgcn_readfirstlane(r[0]);
-  o[1] = __builtin_amdgcn_readfirstlane(r[1]);
-  o[2] = __builtin_amdgcn_readfirstlane(r[2]);
-  o[3] = __builtin_amdgcn_readfirstlane(r[3]);
-  return o;
-}
-__device__ __forceinline__ uint32_t sgpr1(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 // Each lane's 16 (or 4) bytes land at lds_addr + lane * 16 (or 4); the
 // wave's instruction fills 1 KiB (256 B) of LDS contiguously.  Issued as
 // assembly on purpose: the compiler, unable to tell which LDS stage such a
 // load fills, would otherwise wait for every one of them before any LDS
 // read and empty the prefetch ring.  Callers wait with s_waitcnt vmcnt.
+// The descriptor, LDS address and scalar offset must be wave-uniform values
+// the compiler keeps in scalar registers (the assembler rejects the
+// instruction otherwise).
 __device__ __forceinline__ void lds_dma16(u32x4 rsrc, uint32_t lds_addr, uint32_t voff, uint32_t soff) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                :
-               : "s"(sgpr1(lds_addr)), "v"(voff), "s"(sgpr4(rsrc)), "s"(sgpr1(soff))
+               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
                : "memory");
 }
 __device__ __forceinline__ void lds_dma16_nt(u32x4 rsrc, uint32_t lds_addr, uint32_t voff, uint32_t soff) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen nt lds"
                :
-               : "s"(sgpr1(lds_addr)), "v"(voff), "s"(sgpr4(rsrc)), "s"(sgpr1(soff))
+               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
                : "memory");
 }
 __device__ __forceinline__ void lds_dma4(u32x4 rsrc, uint32_t lds_addr, uint32_t voff, uint32_t soff) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
                :
-               : "s"(sgpr1(lds_addr)), "v"(voff), "s"(sgpr4(rsrc)), "s"(sgpr1(soff))
+               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
                : "memory");
 }
 // s_waitcnt constraining only the vector-memory count (gfx9 encoding:

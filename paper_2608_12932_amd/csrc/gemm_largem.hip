@@ -1,30 +1,36 @@
 // Large-M W4A8 GEMM (streaming prefill of new-frame tokens, M > 64).
 //
 // At large M the layer is bound by the INT8 contraction (FlashDrive
-// Sec. 4.2: prefill gains from the INT8 matrix units), so the kernel keeps
+// Sec. 4.2: prefill gains from the INT8 matrix units), so the kernels keep
 // the matrix cores fed:
 //   - a BM x BN output tile per workgroup, 128 k per step (one scale group);
 //     tile sizes are picked on the host so that the tile count fills the 256
 //     CUs in whole waves;
 //   - each step's int8 activation tile and packed int4 weight tile travel
-//     from HBM straight into one stage of an R-deep LDS ring
-//     (buffer_load_dwordx4 ... lds: no registers, no VALU); step kb + R - 1
-//     is issued right after the barrier of step kb, into the stage step
-//     kb - 1 just released, so R - 1 steps of MFMA work cover the latency;
+//     from HBM straight into one stage of a 4-deep LDS ring
+//     (buffer_load_dwordx4 ... lds: no registers, no VALU).  Right after the
+//     barrier of step kb, step kb + 4 refills step kb's stage, whose operands
+//     are already in registers, so three steps of MFMA work cover the load
+//     latency;
 //   - every load instruction writes 1 KiB of LDS contiguously; activation
-//     rows still land XOR-swizzled (16-byte chunk c of row r at c ^ (r & 7),
-//     so the 32 row reads of an MFMA operand hit distinct banks) because each
-//     lane fetches the global chunk that belongs at its LDS position; weight
-//     chunks keep the packed order, which is already conflict free;
-//   - every wave holds a (32 WM) x (32 WN) accumulator tile of
-//     v_mfma_i32_32x32x32_i8 blocks; the weight nibbles are unpacked in
-//     registers right before the MFMAs;
+//     rows land XOR-swizzled (16-byte chunk c of row r at c ^ ((r >> 1) & 7))
+//     because each lane fetches the global chunk that belongs at its LDS
+//     position.  ds_read_b128 serves 16 lanes (256 bytes of banks) per
+//     clock; with 128-byte rows, the 16 rows an operand read touches in one
+//     clock then fall on 16 distinct 16-byte bank groups (a swizzle on r & 7
+//     left rows r and r + 8 on the same banks and halved the read rate).
+//     Weight chunks keep the packed order, already conflict free;
+//   - the operands of step kb + 1 are read from LDS into a second register
+//     set between the MFMAs of step kb (v_mfma_i32_32x32x32_i8), and every
+//     other instruction of a step (stage fill, LDS reads, nibble unpack) is
+//     dealt out evenly between the MFMAs;
 //   - workgroups are renumbered so that the tiles given to one XCD (the
 //     hardware deals workgroups to the 8 XCDs round robin) share their
-//     activation rows in that XCD's L2.
+//     weight columns in that XCD's L2.
 // The epilogue applies per-token and per-channel scales (or, in group mode,
 // each step's int32 partial is rescaled by its fp16 group scale into an
-// fp32 accumulator).
+// fp32 accumulator), stages the output tile in the idle LDS ring and writes
+// it as 16-byte row chunks.
 #include <cstdio>
 #include <type_traits>
 
@@ -36,6 +42,7 @@ namespace w4a8 {
 namespace {
 
 constexpr int kRing = 4;  // LDS stages in flight
+
 
 template <int WM, int WN, int GM, int GN, bool GROUP>
 __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
@@ -84,7 +91,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
   for (int j = 0; j < kACh; ++j) {
     const int p = j * kThreads + tid;
-    const int row = p >> 3, ch = (p & 7) ^ (row & 7);
+    const int row = p >> 3, ch = (p & 7) ^ ((row >> 1) & 7);
     a_voff[j] = (uint32_t)(row * K + ch * 16);
   }
   // group scales: wave w fetches columns [w kSPerWave, +kSPerWave), two per
@@ -114,9 +121,9 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   };
 
   // LDS read offsets of this lane's MFMA operands: activation row
-  // wm 32 WM + 32 i + l32 (its chunks c sit at c ^ (row & 7)), weight column
+  // wm 32 WM + 32 i + l32 (its chunks c sit at c ^ ((row >> 1) & 7)), weight column
   // wn 32 WN + 32 j + l32 of the stage's weight tiles.
-  const int swz = l32 & 7;
+  const int swz = (l32 >> 1) & 7;
   uint32_t a_rd[WM], b_rd[WN];
 #pragma unroll
   for (int i = 0; i < WM; ++i) a_rd[i] = (uint32_t)((wm * 32 * WM + i * 32 + l32) * 128);
@@ -174,9 +181,9 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   // (rows 8 q + 4 g2 + e of block i), one channel scale per column block.
   const bool scaled = a.out_kind != kOutI32;
   const __amdgpu_buffer_rsrc_t xsres =
-      make_rsrc(uniform_ptr(a.x_scale + m0), sgpr1(scaled ? (uint32_t)(rows_here * 4) : 0u));
+      make_rsrc(uniform_ptr(a.x_scale + m0), uniform_u32(scaled ? (uint32_t)(rows_here * 4) : 0u));
   const __amdgpu_buffer_rsrc_t wsres = make_rsrc(uniform_ptr(static_cast<const float*>(a.w_scale) + n0),
-                                                 sgpr1((!GROUP && scaled) ? (uint32_t)(cols_here * 4) : 0u));
+                                                 uniform_u32((!GROUP && scaled) ? (uint32_t)(cols_here * 4) : 0u));
   float swv[WN];
 #pragma unroll
   for (int j = 0; j < WN; ++j)

@@ -256,46 +256,57 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
         for (int r = 0; r < 4; ++r) facc[mt][t][r] = 0.0f;
     }
 
-  for (int base = 0; base < iters; base += D) {
+  // Stage s of the block at base: compute block i = base + s from slot s.
+  auto compute_stage = [&](int s, int i) {
+    v4i alo[MT], ahi[MT];
+    if constexpr (QM == kQLds) {
+      // Rows past M and stages past the split read clamped LDS addresses:
+      // their weights are zero, and rows past M are never stored.
+      const int kb = min(stage_kb(i), kb_end - 1);
+      const uint8_t* p = l_body + min(r16, M - 1) * ldq + (kb - kb_begin) * 128 + g4 * 32;
+      alo[0] = *reinterpret_cast<const v4i*>(p);
+      ahi[0] = *reinterpret_cast<const v4i*>(p + 16);
+    } else {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        alo[mt] = as_v4i(ab[s][mt][0]);
+        ahi[mt] = as_v4i(ab[s][mt][1]);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const v4i blo = nib_lo(wb[s][t]);
+      const v4i bhi = nib_hi(wb[s][t]);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        if constexpr (GROUP) {
+          v4i p = mfma16(alo[mt], blo, zero4);
+          p = mfma16(ahi[mt], bhi, p);
+          const float sg = f16_to_f32(sgb[s][t]) * 0.0625f;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) facc[mt][t][r] = __fmaf_rn((float)p[r], sg, facc[mt][t][r]);
+        } else {
+          acc[mt][t] = mfma16(alo[mt], blo, acc[mt][t]);
+          acc[mt][t] = mfma16(ahi[mt], bhi, acc[mt][t]);
+        }
+      }
+    }
+  };
+  // Blocks with a successor refill each slot right after computing it; the
+  // last block (its slots hold stages base .. base + D - 1, the final ones or
+  // zeros past the split) only computes.  Both loops issue a fixed number
+  // of loads, so the compiler's vmcnt waits stay exact, and no load is
+  // issued for stages that would only read zeros past the end.
+  int base = 0;
+  for (; base + D < iters; base += D) {
 #pragma unroll
     for (int s = 0; s < D; ++s) {
-      const int i = base + s;
-      v4i alo[MT], ahi[MT];
-      if constexpr (QM == kQLds) {
-        // Rows past M and stages past the split read clamped LDS addresses:
-        // their weights are zero, and rows past M are never stored.
-        const int kb = min(stage_kb(i), kb_end - 1);
-        const uint8_t* p = l_body + min(r16, M - 1) * ldq + (kb - kb_begin) * 128 + g4 * 32;
-        alo[0] = *reinterpret_cast<const v4i*>(p);
-        ahi[0] = *reinterpret_cast<const v4i*>(p + 16);
-      } else {
-  #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          alo[mt] = as_v4i(ab[s][mt][0]);
-          ahi[mt] = as_v4i(ab[s][mt][1]);
-        }
-      }
-  #pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        const v4i blo = nib_lo(wb[s][t]);
-        const v4i bhi = nib_hi(wb[s][t]);
-  #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          if constexpr (GROUP) {
-            v4i p = mfma16(alo[mt], blo, zero4);
-            p = mfma16(ahi[mt], bhi, p);
-            const float sg = f16_to_f32(sgb[s][t]) * 0.0625f;
-  #pragma unroll
-            for (int r = 0; r < 4; ++r) facc[mt][t][r] = __fmaf_rn((float)p[r], sg, facc[mt][t][r]);
-          } else {
-            acc[mt][t] = mfma16(alo[mt], blo, acc[mt][t]);
-            acc[mt][t] = mfma16(ahi[mt], bhi, acc[mt][t]);
-          }
-        }
-      }
-      load_stage(s, i + D);
+      compute_stage(s, base + s);
+      load_stage(s, base + s + D);
     }
   }
+#pragma unroll
+  for (int s = 0; s < D; ++s) compute_stage(s, base + s);
 
   // ---- reduce the waves' partial sums through LDS
   lds_barrier();  // every wave is done reading the codes

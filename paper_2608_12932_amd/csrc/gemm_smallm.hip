@@ -96,7 +96,13 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int gid = blockIdx.x / a.S, split = blockIdx.x % a.S;
+  // Workgroups are dealt to the 8 XCDs round robin; renumber them so that
+  // each XCD gets a contiguous range of column groups (its output rows then
+  // share cache lines only at the 7 range boundaries, and its weight tiles
+  // are one contiguous range).
+  int bidx = blockIdx.x;
+  if ((gridDim.x & 7) == 0) bidx = (bidx & 7) * (int)(gridDim.x >> 3) + (bidx >> 3);
+  const int gid = bidx / a.S, split = bidx % a.S;
   const int M = a.M, N = a.N, K = a.K, KB = a.KB;
   const int ntiles = N / 16;
   const int nt0 = gid * NT;

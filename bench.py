@@ -14,6 +14,10 @@ Secondary object: streaming prefill of new-frame tokens through the fused
 QKV projection, M=1024, K=4096, N=6144 (MFMA bound, reported in INT8 TOPS,
 2*M*N*K ops per step), cycling 24 weight copies.
 
+Sweep object: the down projection at verification sizes (M = 1, 4, 16,
+K=12288, N=4096, GB/s) and one decoder layer's four linears with group-128
+fp16 scales (M = 1, 16, 256, 2048; GB/s and TOPS per layer).
+
 Timing: W untimed warmup steps, then exactly K steps between HIP events on
 the launch stream, bracketed by device synchronization.  The dominant
 kernel's average duration for the roofline is timed the same way over its
@@ -75,7 +79,7 @@ class DirectCall:
     sizes), so a step costs one C call: the binding's per-call tensor checks
     would otherwise dominate a ~10 us kernel."""
 
-    def __init__(self, x, wps, w_scale, N, y, x_scale=None, workspace=None, out_kind=0):
+    def __init__(self, x, wps, w_scale, N, y, x_scale=None, workspace=None, out_kind=0, scale_mode=0):
         import ctypes
         import paper_2608_12932_amd as w
 
@@ -89,18 +93,21 @@ class DirectCall:
         self.N = N
         self.y = y.data_ptr()
         self.out_kind = out_kind
-        need = w.w4a8_linear_workspace_bytes(self.M, N, self.K, w.SCALE_CHANNEL_F32, self.in_kind)
+        self.scale_mode = scale_mode
+        need = w.w4a8_linear_workspace_bytes(self.M, N, self.K, scale_mode, self.in_kind)
         self.wk = None
         self.wk_bytes = 0
+        buf = None
         if need:
             buf = workspace.get(need)
             self.wk, self.wk_bytes = buf.data_ptr(), buf.numel()
-        self.keep = (x, wps, w_scale, y, x_scale, workspace)
+        self.keep = (x, wps, w_scale, y, x_scale, buf)
         self.c_size = ctypes.c_size_t
 
     def __call__(self, i, stream):
         rc = self.L.w4a8_linear(self.x, self.in_kind, self.xs, self.M, self.K, self.wps[i % len(self.wps)],
-                                self.ws, 0, self.N, self.y, self.out_kind, self.wk, self.wk_bytes, stream)
+                                self.ws, self.scale_mode, self.N, self.y, self.out_kind,
+                                self.wk, self.wk_bytes, stream)
         if rc:
             raise RuntimeError(f"w4a8_linear failed: {rc}")
 
@@ -198,6 +205,91 @@ def bench_qkv(steps, warmup):
     return dict(M=M, K=K, N=N, ms_step=ms_step, ms_gemm=ms_gemm, ms_quant=ms_quant, ops=ops)
 
 
+def _dev_inputs(key, M, mat_index, copies, cache):
+    """bf16 x, packed weight copies (device clones of one seeded weight, so
+    each step streams distinct addresses), scales and a bf16 y.  The weights
+    are made once per matrix and kept in `cache`."""
+    import torch
+    import paper_2608_12932_amd as w
+    from paper_2608_12932_amd import inputs as I
+
+    wl = I.WORKLOADS[key]
+    name, K, N = wl.mats[mat_index]
+    dev = torch.device("cuda:0")
+    if mat_index not in cache:
+        W, s = I.weights(N, K, I.seed_w(wl.number, 0, name), wl.group)
+        wp0 = w.w4a8_pack_weights(torch.from_numpy(W).to(dev))
+        cache[mat_index] = ([wp0] + [wp0.clone() for _ in range(copies - 1)], torch.from_numpy(s).to(dev))
+    wps, sd = cache[mat_index]
+    x = I.activations(M, K, I.seed_x(wl.number, M), wl.outliers)
+    xd = torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    return xd, wps, sd, y, K, N, sd.numel() * sd.element_size()
+
+
+def bench_down_verify(steps, warmup, copies=16):
+    """Down projection at draft-block verification sizes, K=12288 N=4096,
+    per-channel fp32 scales; 16 weight copies (403 MB) cycled."""
+    import torch
+    import paper_2608_12932_amd as w
+
+    rows, cache = [], {}
+    for M in (1, 4, 16):
+        xd, wps, sd, y, K, N, sbytes = _dev_inputs("down_verify", M, 0, copies, cache)
+        call = DirectCall(xd, wps, sd, N, y, workspace=w.Workspace(xd.device))
+        ms = time_direct(call, steps, warmup)
+        nbytes = N * K // 2 + sbytes + M * K * 2 + M * N * 2
+        rows.append({"M": M, "us_per_step": round(ms * 1e3, 3), "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                     "frac_hbm": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "algorithmic_bytes": nbytes, "kernel": w.w4a8_linear_describe(M, N, K)})
+        del xd, wps, sd, y, call
+    cache.clear()
+    torch.cuda.empty_cache()
+    return {"workload": "down verify (down projection, draft-block verification)", "K": 12288, "N": 4096,
+            "scales": "per-channel fp32", "x": "bf16 in, quantized in the step", "weight_copies": copies,
+            "rows": rows}
+
+
+def bench_layer_group(steps, warmup, copies=6):
+    """One decoder layer's four linears (QKV, O, gate+up, down) with group-128
+    fp16 scales; a step is the four calls, each on its own bf16 x.  Six copies
+    of the layer's weights (580 MB) are cycled."""
+    import torch
+    import paper_2608_12932_amd as w
+    from paper_2608_12932_amd import inputs as I
+
+    rows, cache = [], {}
+    for M in (1, 16, 256, 2048):
+        calls, nbytes, ops, kinds = [], 0, 0, []
+        for mi, (name, K, N) in enumerate(I.LAYER_MATS):
+            xd, wps, sd, y, K, N, sbytes = _dev_inputs("layer_group", M, mi, copies, cache)
+            calls.append(DirectCall(xd, wps, sd, N, y, workspace=w.Workspace(xd.device),
+                                    scale_mode=w.SCALE_GROUP_F16))
+            nbytes += N * K // 2 + sbytes + M * K * 2 + M * N * 2
+            ops += 2 * M * N * K
+            kinds.append(f"{name}: " + w.w4a8_linear_describe(M, N, K, w.SCALE_GROUP_F16))
+        stream = torch.cuda.current_stream().cuda_stream
+
+        def layer(i):
+            for c in calls:
+                c(i, stream)
+
+        n = max(20, steps // (1 if M < 256 else 4 if M == 256 else 16))
+        ms = time_steps(layer, n, max(5, warmup // 4))
+        rows.append({"M": M, "us_per_layer": round(ms * 1e3, 3),
+                     "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                     "frac_hbm": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "TOPS": round(ops / (ms * 1e-3) / 1e12, 2),
+                     "frac_int8": round(ops / (ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
+                     "steps": n, "algorithmic_bytes": nbytes, "ops": ops, "kernels": kinds})
+        del calls
+    cache.clear()
+    torch.cuda.empty_cache()
+    return {"workload": "decoder layer (QKV, O, gate+up, down) with group-128 fp16 scales",
+            "scales": "fp16 per 128 k per channel", "x": "bf16 in, quantized in the step",
+            "layer_copies": copies, "rows": rows}
+
+
 def cpu_baseline(d, algo_bytes, budget_s=10.0):
     """The oracle on the full gate+up verify layer, repeated until about
     budget_s seconds of CPU work have run; the rate is the median run's."""
@@ -224,6 +316,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the down-projection verify and group-scale layer sweeps")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -281,6 +375,9 @@ def main():
                          "kernel": w.w4a8_linear_describe(r["M"], r["N"], r["K"], 0, 1),
                          "traffic": counter_traffic("largem_qkv_prefill")},
         }
+    if not args.no_sweep:
+        ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
+        out["sweep"] = {"down_verify": bench_down_verify(ss, sw), "layer_group": bench_layer_group(ss, sw)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(d, algo_bytes)
     print(json.dumps(out), flush=True)

@@ -22,6 +22,7 @@
 //     own split into LDS, which the waves then read.  In both, the weight
 //     stream is already in flight while the codes are made.
 // The epilogue applies the per-token and per-channel (or per-group) scales.
+#include <cmath>
 #include <cstdio>
 
 #include "device.h"
@@ -363,16 +364,19 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   }
   if (a.S == 1) return;
 
-  // ---- split-K: the last workgroup of this column group finishes
-  __threadfence();
+  // ---- split-K: the last workgroup of this column group finishes.
+  // One agent-scope acquire-release RMW per workgroup, by one thread: the
+  // barrier before it orders every wave's partial stores before the release,
+  // and the barrier after it orders the acquire before every wave's reads.
+  // (A device-scope fence in every wave instead made each call 40-100 us
+  // slower: each one writes back or invalidates the whole L2 of its XCD.)
   __syncthreads();
   if (tid == 0) {
-    const unsigned prev = atomicAdd(&a.counters[gid], 1u);
+    const unsigned prev = __hip_atomic_fetch_add(&a.counters[gid], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     l_last = prev == (unsigned)(a.S - 1);
   }
   __syncthreads();
   if (!l_last) return;
-  __threadfence();
 #pragma unroll
   for (int q = 0; q < kOPT; ++q) {
     const int o = tid + q * kThreads;
@@ -383,16 +387,16 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
     if constexpr (GROUP) {
       const float* part = static_cast<const float*>(a.partial);
       float v = 0.0f;
-      for (int s = 0; s < a.S; ++s) v += __builtin_nontemporal_load(part + ((size_t)s * M + row) * N + n);
+      for (int s = 0; s < a.S; ++s) v += part[((size_t)s * M + row) * N + n];
       emit.group(row, n, v, sxp[q]);
     } else {
       const int* part = static_cast<const int*>(a.partial);
       int v = 0;
-      for (int s = 0; s < a.S; ++s) v += __builtin_nontemporal_load(part + ((size_t)s * M + row) * N + n);
+      for (int s = 0; s < a.S; ++s) v += part[((size_t)s * M + row) * N + n];
       emit.channel(row, n, v, sxp[q], swp[q]);
     }
   }
-  if (tid == 0) atomicExch(&a.counters[gid], 0u);
+  if (tid == 0) __hip_atomic_store(&a.counters[gid], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 typedef void (*SmallMKernel)(const SmallMArgs);
@@ -435,15 +439,31 @@ SmallMKernel pick(const SmallMPlan& p) { return p.group ? pick_group<true>(p) : 
 
 }  // namespace
 
+// Plan cost model, fitted to measurements of the layer shapes at M = 1..16:
+// a call takes about
+//   (rounds - 1) * kRoundUs + max(all bytes / kHbmGBs, rounds * bytes per workgroup / kCuGBs)
+//   + kSplitUs if K is split,
+// where rounds = workgroup rounds over the 256 CUs.  One workgroup streams
+// at most ~60 GB/s, the whole chip ~6.5 TB/s; a second round of workgroups
+// costs its own ramp-up and drain; a K split adds a serial chain (partial
+// stores, the arrival counter, the finishing workgroup's reads).  With the
+// layer shapes this keeps S = 1 (the partial-sum handoff never pays off
+// below ~400 KB of weights per workgroup) and picks the narrowest column
+// group that still fits one round.
+constexpr double kRoundUs = 1.5;
+constexpr double kHbmGBs = 6500.0;
+constexpr double kCuGBs = 60.0;
+constexpr double kSplitUs = 5.0;
+
 SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in) {
   SmallMPlan p{};
   p.MT = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   p.group = group;
   const int ntiles = N / 16, KB = K / 128;
-  const double ideal = (double)ntiles * KB / 256.0;  // blocks per CU if perfectly spread
-  const int nts[] = {6, 4, 3, 2, 1};
-  const int ss[] = {1, 2, 3, 4, 6, 8};
-  double best = -1.0;
+  const int nts[] = {1, 2, 3, 4, 6};
+  const int ss[] = {1, 2, 4, 8};
+  const double all_bytes = (double)N * K / 2;
+  double best = 1e30;
   for (int nt : nts) {
     if (ntiles % nt || p.MT * nt > kMaxTilesPerWave) continue;
     // the int8-input group kernels hold at most kMaxGroupTiles tiles (the
@@ -452,13 +472,16 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in) {
     for (int s : ss) {
       if (s > KB) continue;
       const int kbs = (KB + s - 1) / s;
-      const int wgs = ntiles / nt * s;
-      const double per_cu = (double)((wgs + 255) / 256) * nt * kbs;
-      double score = ideal / per_cu;
-      if (s > 1) score /= 1.0 + (double)s * M * N * 8.0 / ((double)N * K / 2.0);
-      // prefer fewer workgroups on a tie (less redundant activation traffic)
-      if (score > best + 1e-9 || (score > best - 1e-9 && wgs < p.groups * p.S)) {
-        best = score;
+      const long wgs = (long)(ntiles / nt) * s;
+      const long rounds = (wgs + 255) / 256;
+      // weights, plus the activation codes every workgroup reads (from L2,
+      // counted at half weight)
+      const double wg_bytes = (double)nt * kbs * kBlockBytes + 0.5 * (double)M * kbs * 128;
+      double us = (double)(rounds - 1) * kRoundUs +
+                  fmax(all_bytes / (kHbmGBs * 1e3), (double)rounds * wg_bytes / (kCuGBs * 1e3));
+      if (s > 1) us += kSplitUs;
+      if (us < best - 1e-9) {
+        best = us;
         p.NT = nt;
         p.S = s;
         p.groups = ntiles / nt;
@@ -469,12 +492,13 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in) {
   int mp = 1;
   while (mp < M) mp *= 2;
   p.tpr = kThreads / (mp < 16 ? mp : 16);
-  // Fused quantize only for narrow column groups: with NT >= 3 the waves'
-  // deeper weight prologue stalls them at issue while the quantize work is
-  // still ahead, and a separate quantize kernel is faster (measured on the
-  // gate+up and down verification shapes, M = 1..16).
+  // Fused quantize only for narrow column groups over a long K: with NT >= 3
+  // the waves' deeper weight prologue stalls them at issue while the
+  // quantize work is still ahead, and with K < 8192 the activation read
+  // every workgroup makes before its weight stream costs more than the
+  // separate quantize launch (measured on the layer shapes, M = 1..16).
   p.qmode = kQNone;
-  if (bf16_in && p.MT == 1 && p.NT <= kMaxFusedTiles && (K / 8) % p.tpr == 0 &&
+  if (bf16_in && p.MT == 1 && p.NT <= kMaxFusedTiles && KB >= 64 && (K / 8) % p.tpr == 0 &&
       (K / 8) / p.tpr <= kXCache && (size_t)M * (kbs * 128 + 16) <= 96 * 1024)
     p.qmode = kQLds;
   p.fused = p.qmode != kQNone;

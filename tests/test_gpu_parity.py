@@ -146,14 +146,18 @@ def test_group_scales(M, K, N):
 
 # ------------------------------------------------------------ split-K, determinism, workspace reuse
 
-def test_split_k_paths_and_reuse():
-    # few output tiles and a long K make the planner split K across workgroups
+@pytest.mark.parametrize("M,N", [(16, 32), (1, 16)])
+def test_split_k_paths_and_reuse(M, N):
+    # one or two output tiles over the longest supported K make the planner
+    # split K across workgroups (with the quantize separate at M = 16 and
+    # fused at M = 1)
     for group in (False, True):
-        M, K, N = 16, 8192, 128
+        K = 65536
         desc = w.w4a8_linear_describe(M, N, K, int(group))
         assert "S=1 " not in desc, desc
-        x = I.activations(M, K, 700)
-        W, s = I.weights(N, K, 701, group=group)
+        assert ("fused-quant" in desc) == (M == 1), desc
+        x = I.activations(M, K, 700 + M)
+        W, s = I.weights(N, K, 701 + N, group=group)
         ref = check_all_outputs(x, W, s, group=group, label="split-K")
         ws = w.Workspace()
         wp = pack(W)

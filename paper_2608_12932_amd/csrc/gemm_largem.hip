@@ -266,7 +266,12 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
       // MFMA q: k half tp, nibble half h, block (i, j)
       const int tp = q / (2 * WM * WN), h = (q / (WM * WN)) % 2, i = (q / WN) % WM, j = q % WN;
       const v4i& bop = tp == 0 ? (h ? cur.hi0[j] : cur.lo0[j]) : (h ? hi1[j] : lo1[j]);
-      c[i][j] = mfma32(cur.a[i][2 * tp + h], bop, c[i][j]);
+      // group mode: a step's first MFMA into a block starts from zero (an
+      // inline constant), so the rescaled partial needs no clearing
+      if (GROUP && tp == 0 && h == 0)
+        c[i][j] = mfma32(cur.a[i][2 * tp + h], bop, v16i{});
+      else
+        c[i][j] = mfma32(cur.a[i][2 * tp + h], bop, c[i][j]);
 #pragma unroll
       for (int d = 0; d < kPerStage; ++d)
         if (d * kMfma / kPerStage == q) issue_one(kb + kRing, d);
@@ -284,7 +289,6 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
           const int e = q * (kRescale / kMfma) + t;
           const int ri = e / (WN * 16), rj = (e / 16) % WN, rr = e % 16;
           facc[ri][rj][rr] = __fmaf_rn((float)prev[ri][rj][rr], sg_prev[rj], facc[ri][rj][rr]);
-          prev[ri][rj][rr] = 0;
         }
       }
       __builtin_amdgcn_sched_barrier(0);

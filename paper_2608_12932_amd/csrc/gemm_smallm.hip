@@ -39,7 +39,6 @@ constexpr int kOperandVgprs = 128;   // registers for in-flight weight (+ activa
 constexpr int kOperandVgprsFused = 112;  // the fused path also holds the x chunks
 constexpr int kLdsHeader = 256;   // per-row absmax / s / inv / mode
 constexpr int kMaxTilesPerWave = 12;
-constexpr int kMaxGroupTiles = 3;  // int8-input group kernels: more tiles spill
 constexpr int kMaxFusedTiles = 2;  // fused quantize pays off up to this many tiles
 
 // How the activations reach the MFMA A operand.
@@ -405,8 +404,7 @@ typedef void (*SmallMKernel)(const SmallMArgs);
 // and in-flight operands no longer fit in 256 registers.
 template <int MT, int NT, bool GROUP, int QM>
 SmallMKernel instance() {
-  if constexpr (MT * NT <= kMaxTilesPerWave && (QM != kQNone || !GROUP || NT <= kMaxGroupTiles) &&
-                (QM == kQNone || MT == 1))
+  if constexpr (MT * NT <= kMaxTilesPerWave && (QM == kQNone || MT == 1))
     return smallm<MT, NT, GROUP, QM>;
   else
     return nullptr;
@@ -466,9 +464,6 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in) {
   double best = 1e30;
   for (int nt : nts) {
     if (ntiles % nt || p.MT * nt > kMaxTilesPerWave) continue;
-    // the int8-input group kernels hold at most kMaxGroupTiles tiles (the
-    // fused decision is taken below, so stay within the tighter bound)
-    if (group && nt > kMaxGroupTiles) continue;
     for (int s : ss) {
       if (s > KB) continue;
       const int kbs = (KB + s - 1) / s;

@@ -1,0 +1,22 @@
+// Group-scale instances of the large-M W4A8 GEMM (largem_kernel.h).
+//
+// This file is built with -mllvm -amdgpu-mfma-vgpr-form: the MFMAs then
+// write their int32 partial sums to VGPRs, where the per-step rescale reads
+// them directly (from AGPRs every element would first need a
+// v_accvgpr_read, one more VALU instruction per element and step in a loop
+// that is bound by its VALU work).  The per-channel instances keep the
+// default AGPR form, which is faster for them.
+#include "largem_kernel.h"
+
+namespace w4a8 {
+
+LargeMKernelFn largem_group_kernel(int cfg) {
+  switch (cfg) {
+    case 1: return largem<2, 2, 2, 2, true>;
+    case 2: return largem<1, 3, 2, 1, true>;
+    case 3: return largem<1, 1, 2, 2, true>;
+    default: return nullptr;  // 128 x 192 does not fit the group accumulators
+  }
+}
+
+}  // namespace w4a8

@@ -68,6 +68,10 @@ struct LargeMPlan {
 };
 LargeMPlan plan_largem(int M, int N, int K, bool group);
 hipError_t launch_largem(const LargeMPlan& p, const LargeMArgs& a, hipStream_t stream);
+typedef void (*LargeMKernelFn)(const LargeMArgs);
+// group-scale instance of tile-menu entry cfg (gemm_largem_group.hip), or
+// nullptr where the tile does not fit the group accumulators
+LargeMKernelFn largem_group_kernel(int cfg);
 
 const char* smallm_kernel_name(const SmallMPlan& p);
 const char* largem_kernel_name(const LargeMPlan& p);

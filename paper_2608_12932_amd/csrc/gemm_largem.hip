@@ -9,26 +9,12 @@ namespace w4a8 {
 
 namespace {
 
-struct TileCfg {
-  int WM, WN, GM, GN;
-  double quality;  // relative efficiency of the tile shape (operand reuse)
-  bool group_ok;   // fits the registers with group-mode accumulators
-};
-// BM = 32 WM GM, BN = 32 WN GN
-constexpr TileCfg kMenu[] = {
-    {2, 3, 2, 2, 1.00, false},  // 128 x 192, 4 waves
-    {2, 2, 2, 2, 0.95, true},   // 128 x 128, 4 waves
-    {1, 3, 2, 1, 0.85, true},   // 64 x 96, 2 waves
-    {1, 1, 2, 2, 0.70, true},   // 64 x 64, 4 waves
-};
-constexpr int kMenuSize = sizeof(kMenu) / sizeof(kMenu[0]);
-
 LargeMKernelFn channel_kernel(int cfg) {
   switch (cfg) {
-    case 0: return largem<2, 3, 2, 2, false>;
-    case 1: return largem<2, 2, 2, 2, false>;
-    case 2: return largem<1, 3, 2, 1, false>;
-    case 3: return largem<1, 1, 2, 2, false>;
+    case 0: return menu_kernel<0, false>();
+    case 1: return menu_kernel<1, false>();
+    case 2: return menu_kernel<2, false>();
+    case 3: return menu_kernel<3, false>();
     default: return nullptr;
   }
 }
@@ -59,8 +45,8 @@ LargeMPlan plan_largem(int M, int N, int K, bool group) {
       p.tiles_n = tn;
     }
   }
-  p.lds_bytes = kRing * ((size_t)p.BM * 128 + (size_t)p.BN / 16 * kBlockBytes +
-                          (group ? (size_t)p.threads / 64 * 256 : 0));
+  p.lds_bytes = (size_t)kMenu[p.cfg].ring * ((size_t)p.BM * 128 + (size_t)p.BN / 16 * kBlockBytes +
+                                             (group ? (size_t)p.threads / 64 * 256 : 0));
   return p;
 }
 

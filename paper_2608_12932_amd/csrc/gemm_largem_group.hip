@@ -12,9 +12,9 @@ namespace w4a8 {
 
 LargeMKernelFn largem_group_kernel(int cfg) {
   switch (cfg) {
-    case 1: return largem<2, 2, 2, 2, true>;
-    case 2: return largem<1, 3, 2, 1, true>;
-    case 3: return largem<1, 1, 2, 2, true>;
+    case 1: return menu_kernel<1, true>();
+    case 2: return menu_kernel<2, true>();
+    case 3: return menu_kernel<3, true>();
     default: return nullptr;  // 128 x 192 does not fit the group accumulators
   }
 }

@@ -43,10 +43,23 @@ namespace w4a8 {
 
 namespace {
 
-constexpr int kRing = 4;  // LDS stages in flight
+// The tile menu: BM = 32 WM GM rows, BN = 32 WN GN columns, ring = LDS
+// stages in flight.  The small tiles' stages are small, so they keep more of
+// them in flight to cover the L2 latency.
+struct TileCfg {
+  int WM, WN, GM, GN, ring;
+  double quality;  // relative efficiency of the tile shape (operand reuse)
+  bool group_ok;   // fits the registers with group-mode accumulators
+};
+constexpr TileCfg kMenu[] = {
+    {2, 3, 2, 2, 4, 1.00, false},  // 128 x 192, 4 waves
+    {2, 2, 2, 2, 4, 0.95, true},   // 128 x 128, 4 waves
+    {1, 3, 2, 1, 4, 0.85, true},   // 64 x 96, 2 waves
+    {1, 1, 2, 2, 4, 0.70, true},   // 64 x 64, 4 waves
+};
+constexpr int kMenuSize = sizeof(kMenu) / sizeof(kMenu[0]);
 
-
-template <int WM, int WN, int GM, int GN, bool GROUP>
+template <int WM, int WN, int GM, int GN, bool GROUP, int kRing>
 __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   constexpr int kThreads = GM * GN * 64;
   constexpr int kWaves = GM * GN;
@@ -500,6 +513,12 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
     store_tile(std::integral_constant<int, 2>{});
   else
     store_tile(std::integral_constant<int, 4>{});
+}
+
+// The instance of menu entry C.
+template <int C, bool GROUP>
+constexpr LargeMKernelFn menu_kernel() {
+  return largem<kMenu[C].WM, kMenu[C].WN, kMenu[C].GM, kMenu[C].GN, GROUP, kMenu[C].ring>;
 }
 
 }  // namespace

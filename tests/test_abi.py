@@ -69,6 +69,25 @@ def test_plans_fill_the_chip():
     assert "groups=256" in d
 
 
+def test_split_and_fusion_choices():
+    # K is split across workgroups only where one workgroup's weight stream
+    # would be long (one or two column tiles over K = 65536), never at the
+    # decoder-layer shapes; the quantize is fused only for narrow column
+    # groups over a long K.
+    for K, N in ((4096, 6144), (4096, 4096), (4096, 24576), (12288, 4096)):
+        for M in (1, 4, 16, 64):
+            for mode in (0, 1):
+                assert "S=1 " in w.w4a8_linear_describe(M, N, K, mode), (M, N, K, mode)
+    for M in (1, 16):
+        assert "S=8 " in w.w4a8_linear_describe(M, 16, 65536)
+    assert "fused-quant" in w.w4a8_linear_describe(1, 4096, 12288)
+    assert "fused-quant" in w.w4a8_linear_describe(4, 4096, 12288, 1)
+    assert "fused-quant" not in w.w4a8_linear_describe(1, 4096, 4096)
+    assert "fused-quant" not in w.w4a8_linear_describe(16, 6144, 4096)
+    # group scales use the same column groups as per-channel scales
+    assert "NT=6" in w.w4a8_linear_describe(16, 24576, 4096, 1)
+
+
 def test_malformed_calls_are_rejected_without_launch():
     L = w.lib()
     P = ctypes.c_void_p

@@ -319,6 +319,8 @@ def main():
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the down-projection verify and group-scale layer sweeps")
+    ap.add_argument("--sweep-only", action="store_true",
+                    help="run only the sweeps (for profiling their kernels); prints the sweep object")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -330,6 +332,11 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     w.lib()
+    if args.sweep_only:
+        ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
+        print(json.dumps({"sweep": {"down_verify": bench_down_verify(ss, sw),
+                                    "layer_group": bench_layer_group(ss, sw)}}), flush=True)
+        return
     d, ms, algo_bytes, ms_gemm, gemm_bytes = bench_gate_up(args.steps, args.warmup)
     gbs = algo_bytes / (ms * 1e-3) / 1e9
     gemm_gbs = gemm_bytes / (ms_gemm * 1e-3) / 1e9

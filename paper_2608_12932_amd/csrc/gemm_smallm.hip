@@ -35,7 +35,13 @@ namespace {
 constexpr int kWaves = kSmallMWaves;
 constexpr int kThreads = kWaves * 64;
 constexpr int kXCache = 16;       // fused quantize: x chunks held per thread
-constexpr int kOperandVgprs = 128;   // registers for in-flight weight (+ activation) stages
+// Registers for in-flight weight (+ activation) stages.  Narrow column
+// groups (NT <= 2) get more, so a long K split (K = 12288: 12 blocks per
+// wave) fits in one block of stages; wider groups already hold a whole
+// K = 4096 split, and a deeper ring only costs them registers.  Group mode
+// also holds the fp32 sums and the stage scales.
+constexpr int kOperandVgprsNarrow = 152;
+constexpr int kOperandVgprs = 128;
 constexpr int kOperandVgprsFused = 112;  // the fused path also holds the x chunks
 constexpr int kLdsHeader = 256;   // per-row absmax / s / inv / mode
 constexpr int kMaxTilesPerWave = 12;
@@ -47,10 +53,10 @@ enum QMode {
   kQLds = 1,   // bf16 in; codes made in LDS
 };
 
-template <int MT, int NT, int QM>
-constexpr int stage_depth() {
+// Weight stages in flight per wave (used by the kernels and the planner).
+constexpr int stage_depth(int MT, int NT, int QM, bool GROUP) {
   int per = NT * 4 + (QM == kQLds ? 0 : MT * 8);
-  int d = (QM == kQLds ? kOperandVgprsFused : kOperandVgprs) / per;
+  int d = (QM == kQLds ? kOperandVgprsFused : !GROUP && NT <= 2 ? kOperandVgprsNarrow : kOperandVgprs) / per;
   return d < 1 ? 1 : (d > 16 ? 16 : d);
 }
 
@@ -82,10 +88,10 @@ struct Emit {
   }
 };
 
-template <int MT, int NT, bool GROUP, int QM>
+template <int MT, int NT, bool GROUP, int QM, bool EXACT>
 __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   constexpr bool FUSED = QM != kQNone;
-  constexpr int D = stage_depth<MT, NT, QM>();
+  constexpr int D = stage_depth(MT, NT, QM, GROUP);
   extern __shared__ __align__(16) uint8_t lds[];
   uint32_t* l_amax = reinterpret_cast<uint32_t*>(lds);
   float* l_s = reinterpret_cast<float*>(lds + 64);
@@ -176,9 +182,14 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
     }
   };
   // Without the LDS-mode quantize the whole prologue is issued at once.
+  // Stages past this wave's last block are not issued (nor computed below):
+  // with a short split, D can exceed the blocks a wave owns.  Group mode
+  // issues them (they read zeros): guarding its loads made the compiler
+  // spill the stage registers.
   if constexpr (QM != kQLds) {
 #pragma unroll
-    for (int s = 0; s < D; ++s) load_stage(s, s);
+    for (int s = 0; s < D; ++s)
+      if (EXACT || GROUP || s < iters) load_stage(s, s);
   }
 
   // ---- epilogue scales, fetched now so their latency hides under the
@@ -232,7 +243,7 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
     constexpr int kPer = (kXCache + D - 1) / D;  // chunks quantized after each stage
 #pragma unroll
     for (int st = 0; st < D; ++st) {
-      load_stage(st, st);
+      if (EXACT || GROUP || st < iters) load_stage(st, st);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int jj = 0; jj < kPer; ++jj) {
@@ -299,20 +310,26 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
     }
   };
   // Blocks with a successor refill each slot right after computing it; the
-  // last block (its slots hold stages base .. base + D - 1, the final ones or
-  // zeros past the split) only computes.  Both loops issue a fixed number
-  // of loads, so the compiler's vmcnt waits stay exact, and no load is
-  // issued for stages that would only read zeros past the end.
+  // last block (its slots hold stages base .. base + D - 1) only computes.
+  // Stages at or past iters are not computed, and in channel mode not
+  // loaded either (wave-uniform branches): they would only read and
+  // multiply zeros, which cost 9-14 % where D exceeds a wave's blocks
+  // (K = 4096 at NT <= 2, K = 12288).
+  // EXACT instances (the host picks them when every wave's block count is a
+  // multiple of D, e.g. gate+up: 4 blocks per wave, 4 stages) run the loop
+  // without the branches, which split the compiler's scheduling regions and
+  // cost ~2 % there.
   int base = 0;
   for (; base + D < iters; base += D) {
 #pragma unroll
     for (int s = 0; s < D; ++s) {
       compute_stage(s, base + s);
-      load_stage(s, base + s + D);
+      if (EXACT || GROUP || base + s + D < iters) load_stage(s, base + s + D);
     }
   }
 #pragma unroll
-  for (int s = 0; s < D; ++s) compute_stage(s, base + s);
+  for (int s = 0; s < D; ++s)
+    if (EXACT || base + s < iters) compute_stage(s, base + s);
 
   // ---- reduce the waves' partial sums through LDS
   lds_barrier();  // every wave is done reading the codes
@@ -403,32 +420,32 @@ typedef void (*SmallMKernel)(const SmallMArgs);
 // MT * NT is capped at 12 (kMaxTilesPerWave): beyond it the accumulators
 // and in-flight operands no longer fit in 256 registers.
 template <int MT, int NT, bool GROUP, int QM>
-SmallMKernel instance() {
+SmallMKernel instance(bool exact) {
   if constexpr (MT * NT <= kMaxTilesPerWave && (QM == kQNone || MT == 1))
-    return smallm<MT, NT, GROUP, QM>;
+    return exact ? smallm<MT, NT, GROUP, QM, true> : smallm<MT, NT, GROUP, QM, false>;
   else
     return nullptr;
 }
 
 template <int MT, bool GROUP, int QM>
-SmallMKernel pick_nt(int NT) {
+SmallMKernel pick_nt(int NT, bool exact) {
   switch (NT) {
-    case 1: return instance<MT, 1, GROUP, QM>();
-    case 2: return instance<MT, 2, GROUP, QM>();
-    case 3: return instance<MT, 3, GROUP, QM>();
-    case 4: return instance<MT, 4, GROUP, QM>();
-    case 6: return instance<MT, 6, GROUP, QM>();
+    case 1: return instance<MT, 1, GROUP, QM>(exact);
+    case 2: return instance<MT, 2, GROUP, QM>(exact);
+    case 3: return instance<MT, 3, GROUP, QM>(exact);
+    case 4: return instance<MT, 4, GROUP, QM>(exact);
+    case 6: return instance<MT, 6, GROUP, QM>(exact);
     default: return nullptr;
   }
 }
 
 template <bool GROUP>
 SmallMKernel pick_group(const SmallMPlan& p) {
-  if (p.qmode == kQLds) return pick_nt<1, GROUP, kQLds>(p.NT);
+  if (p.qmode == kQLds) return pick_nt<1, GROUP, kQLds>(p.NT, p.exact);
   switch (p.MT) {
-    case 1: return pick_nt<1, GROUP, kQNone>(p.NT);
-    case 2: return pick_nt<2, GROUP, kQNone>(p.NT);
-    case 4: return pick_nt<4, GROUP, kQNone>(p.NT);
+    case 1: return pick_nt<1, GROUP, kQNone>(p.NT, p.exact);
+    case 2: return pick_nt<2, GROUP, kQNone>(p.NT, p.exact);
+    case 4: return pick_nt<4, GROUP, kQNone>(p.NT, p.exact);
     default: return nullptr;
   }
 }
@@ -497,6 +514,16 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in) {
       (K / 8) / p.tpr <= kXCache && (size_t)M * (kbs * 128 + 16) <= 96 * 1024)
     p.qmode = kQLds;
   p.fused = p.qmode != kQNone;
+  // Every split's waves own a multiple of D blocks: the loop needs no
+  // guards (the last split may be shorter).  Group kernels always take the
+  // guarded loop, which measured faster for them even where no stage is
+  // skipped (gate+up, M = 1 and 16).
+  {
+    const int D = stage_depth(p.MT, p.NT, p.qmode, group);
+    const int last = KB - (p.S - 1) * kbs;
+    const int it_full = (kbs + kWaves - 1) / kWaves, it_last = (last + kWaves - 1) / kWaves;
+    p.exact = !group && it_full % D == 0 && it_last % D == 0;
+  }
   const size_t red = (size_t)kWaves * p.MT * p.NT * 1024;
   const size_t codes = p.qmode == kQLds ? (size_t)M * (kbs * 128 + 16) : 0;
   p.lds_bytes = kLdsHeader + (red > codes ? red : codes);

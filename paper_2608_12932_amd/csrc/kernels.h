@@ -30,6 +30,7 @@ struct SmallMArgs {
   int M, N, K, KB;
   int S, kbs;            // K splits and 128-k blocks per split
   int tpr;               // fused quantize: threads per token row
+  bool exact;            // every wave's block count is a multiple of the stage depth
   int out_kind;
 };
 struct SmallMPlan {
@@ -40,6 +41,7 @@ struct SmallMPlan {
   bool group;            // group-wise scales
   int groups;            // workgroups along N
   int tpr;               // fused quantize: threads per token row
+  bool exact;            // every wave's block count is a multiple of the stage depth
   size_t lds_bytes;
 };
 SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in);

@@ -19,6 +19,23 @@ REL = 1e-2
 GROUP_FLOOR = 1e-4
 
 
+# (label, shape, scales, max elementwise and normwise relative error of the
+# bf16 output against the oracle's fp64 value); printed in the terminal
+# summary by conftest.py
+ERROR_REPORT = []
+
+
+def record_errors(label, shape, group, y, y64):
+    """Max elementwise relative error over nonzero reference values, and
+    the normwise ||y - y64|| / ||y64||."""
+    y = y.astype(np.float64)
+    nz = y64 != 0
+    max_rel = float(np.max(np.abs(y[nz] - y64[nz]) / np.abs(y64[nz]))) if nz.any() else 0.0
+    den = float(np.linalg.norm(y64))
+    norm_rel = float(np.linalg.norm(y - y64)) / den if den > 0 else float(np.linalg.norm(y - y64))
+    ERROR_REPORT.append((label, shape, "group" if group else "channel", max_rel, norm_rel))
+
+
 def dev():
     return torch.device("cuda:0")
 
@@ -78,6 +95,7 @@ def check_all_outputs(x_bits, W, s, *, group, codes=False, ref=None, rows=None, 
     y32 = run_linear(x_bits, wp, s, N, group=group, out_kind=w.OUT_F32, codes=cq)
     yb = run_linear(x_bits, wp, s, N, group=group, out_kind=w.OUT_BF16, codes=cq)
     y32, yb = y32[sel], yb[sel]
+    record_errors(label, (M, K, N), group, (yb.astype(np.uint32) << 16).view(np.float32), ref["y64"])
     if not group:
         np.testing.assert_array_equal(y32.view(np.uint32), ref["y32"].view(np.uint32),
                                       err_msg=f"{label}: fp32 dequant")

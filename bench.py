@@ -291,6 +291,47 @@ def bench_layer_group(steps, warmup, copies=6):
             "layer_copies": copies, "rows": rows}
 
 
+def measure_ceilings():
+    """Measured HBM-read and INT8-MFMA ceilings (libw4a8_ceiling.so): a plain
+    16-byte streaming read of 1 GiB, and independent 32x32x32 int8 MFMA
+    chains with register operands."""
+    import ctypes
+    import torch
+
+    L = ctypes.CDLL(os.path.join(ROOT, "paper_2608_12932_amd", "libw4a8_ceiling.so"))
+    L.w4a8_ceiling_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
+    L.w4a8_ceiling_mfma_i8.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    st = torch.cuda.current_stream().cuda_stream
+    nbytes = 1 << 30
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    buf.fill_(7)
+    sink = torch.empty(256 * 512, dtype=torch.int32, device="cuda")
+
+    def read(i):
+        if L.w4a8_ceiling_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(), st):
+            raise RuntimeError("ceiling read launch failed")
+
+    ms_read = time_steps(read, 10, 2)
+    iters = 2048
+    msink = torch.empty(1024 * 256, dtype=torch.int32, device="cuda")
+
+    def mfma(i):
+        if L.w4a8_ceiling_mfma_i8(iters, msink.data_ptr(), st):
+            raise RuntimeError("ceiling mfma launch failed")
+
+    ms_mfma = time_steps(mfma, 5, 1)
+    ops = 1024 * 4 * 4 * iters * 65536
+    del buf
+    torch.cuda.empty_cache()
+    gbs = nbytes / (ms_read * 1e-3) / 1e9
+    tops = ops / (ms_mfma * 1e-3) / 1e12
+    return {"hbm_read": {"value": round(gbs, 1), "unit": "GB/s", "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+                         "what": "16-byte non-temporal streaming read of 1 GiB, 256 workgroups x 512 threads, "
+                                 "one contiguous range each"},
+            "int8_mfma": {"value": round(tops, 1), "unit": "TOPS", "frac_of_peak": round(tops / INT8_PEAK_TOPS, 4),
+                          "what": "4 independent v_mfma_i32_32x32x32_i8 chains per wave, 4096 waves"}}
+
+
 def cpu_baseline(d, algo_bytes, budget_s=10.0):
     """The oracle on the full gate+up verify layer, repeated until about
     budget_s seconds of CPU work have run; the rate is the median run's."""
@@ -383,6 +424,7 @@ def main():
                          "kernel": w.w4a8_linear_describe(r["M"], r["N"], r["K"], 0, 1),
                          "traffic": counter_traffic("largem_qkv_prefill")},
         }
+    out["ceilings"] = measure_ceilings()
     if not args.no_sweep:
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
         out["sweep"] = {"down_verify": bench_down_verify(ss, sw), "layer_group": bench_layer_group(ss, sw)}

@@ -12,10 +12,18 @@ import paper_2608_12932_amd as w
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def declared_functions():
-    text = open(os.path.join(ROOT, "include", "w4a8.h")).read()
+def declared_functions(header="w4a8.h"):
+    text = open(os.path.join(ROOT, "include", header)).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(w4a8_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_ceiling_library_exports_every_declared_symbol():
+    L = ctypes.CDLL(os.path.join(ROOT, "paper_2608_12932_amd", "libw4a8_ceiling.so"))
+    names = declared_functions("w4a8_ceiling.h")
+    assert names == ["w4a8_ceiling_mfma_i8", "w4a8_ceiling_stream_read"]
+    for name in names:
+        assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
 
 
 def test_header_declares_the_binding_names():

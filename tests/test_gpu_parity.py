@@ -245,3 +245,26 @@ def test_nan_and_inf_scales():
         y32 = run_linear(x, wp, s, N, group=False, out_kind=w.OUT_F32, codes=(q, sx))
         np.testing.assert_array_equal(y32, ref["y32"], err_msg=f"M={M}: fp32 with non-finite scales")
         assert np.isnan(y32[:, 3]).all() and np.isnan(y32[2]).all() and np.isnan(y32[:, 5]).all()
+
+
+@pytest.mark.parametrize("M", [8, 300, 1024])
+def test_token_scales_at_the_epilogue_bounds(M):
+    # Token scales on both sides of every bound the large-M epilogue's fast
+    # path checks (0, subnormal, 2^-123 / 2^-122, 2^100 / 2^101, negative,
+    # near the fp32 maximum) must give the reference bits in every output
+    # mode; rows are arranged so that some waves see only in-range scales.
+    K, N = 512, 320
+    x = I.activations(M, K, 903)
+    W, s = I.weights(N, K, 904)
+    q, sx = oracle.quantize_act(x)
+    sx = sx.copy()
+    special = np.array([0.0, 2.0**-130, 2.0**-123, 2.0**-122, 2.0**100, 2.0**101, -2.0**-122, -0.75,
+                        3.0e38, 1.5e-30], np.float32)
+    rows = np.arange(0, M, max(1, M // 40))[: special.size]
+    sx[rows] = special[: rows.size]
+    ref = oracle.linear_q(q, sx, W, s_w=s, nthreads=NTHREADS)
+    wp = pack(W)
+    yb = run_linear(x, wp, s, N, group=False, out_kind=w.OUT_BF16, codes=(q, sx))
+    np.testing.assert_array_equal(yb, ref["y"], err_msg=f"M={M}: bf16 at the scale bounds")
+    y32 = run_linear(x, wp, s, N, group=False, out_kind=w.OUT_F32, codes=(q, sx))
+    np.testing.assert_array_equal(y32.view(np.uint32), ref["y32"].view(np.uint32), err_msg=f"M={M}: fp32")

@@ -268,3 +268,20 @@ def test_token_scales_at_the_epilogue_bounds(M):
     np.testing.assert_array_equal(yb, ref["y"], err_msg=f"M={M}: bf16 at the scale bounds")
     y32 = run_linear(x, wp, s, N, group=False, out_kind=w.OUT_F32, codes=(q, sx))
     np.testing.assert_array_equal(y32.view(np.uint32), ref["y32"].view(np.uint32), err_msg=f"M={M}: fp32")
+
+
+@pytest.mark.parametrize("group", [False, True])
+def test_large_m_longest_k(group):
+    # K = 65536 (512 scale groups) on the large-M path: the closed-form
+    # extreme x = +-1, W = -8 gives acc = -+1016 K (16 acc stays below 2^31),
+    # and random rows match the oracle.
+    M, K, N = 80, 65536, 64
+    xs = np.stack([I.to_bf16_bits(np.ones(K, np.float32)), I.to_bf16_bits(-np.ones(K, np.float32))])
+    x = I.activations(M, K, 905)
+    x[:2] = xs
+    W, s = I.weights(N, K, 906, group=group)
+    W = W.copy()
+    W[:8] = -8
+    assert "largem" in w.w4a8_linear_describe(M, N, K, int(group))
+    ref = check_all_outputs(x, W, s, group=group, label="large-M K=65536")
+    assert (ref["acc"][0, :8] == -1016 * K).all() and (ref["acc"][1, :8] == 1016 * K).all()

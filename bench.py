@@ -291,6 +291,61 @@ def bench_layer_group(steps, warmup, copies=6):
             "layer_copies": copies, "rows": rows}
 
 
+def bench_stack(steps, layers=36):
+    """The backbone's W4A8 linears for one decode/verify step: 36 decoder
+    layers x (QKV, O, gate+up, down) with group-128 fp16 scales, each call on
+    its own bf16 x, at M = 1 and 16 tokens.  Weights are device clones of
+    one seeded layer (3.5 GB of distinct addresses, far past the 256 MB
+    Infinity Cache).  Timed as eager calls on torch's stream and as the
+    replay of one captured HIP graph of the whole stack."""
+    import torch
+    import paper_2608_12932_amd as w
+    from paper_2608_12932_amd import inputs as I
+
+    dev = torch.device("cuda:0")
+    base = []
+    for mi, (name, K, N) in enumerate(I.LAYER_MATS):
+        W, sc = I.weights(N, K, I.seed_w(5, 0, name), group=True)
+        base.append((name, K, N, w.w4a8_pack_weights(torch.from_numpy(W).to(dev)), torch.from_numpy(sc).to(dev)))
+    weights = [[(name, K, N, wp if l == 0 else wp.clone(), sc) for (name, K, N, wp, sc) in base] for l in range(layers)]
+    rows = []
+    for M in (1, 16):
+        calls, nbytes = [], 0
+        for l in range(layers):
+            for mi, (name, K, N, wp, sc) in enumerate(weights[l]):
+                x = I.activations(M, K, I.seed_x(5, M) + 7 * l + mi)
+                xd = torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+                y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+                calls.append(DirectCall(xd, [wp], sc, N, y, workspace=w.Workspace(dev), scale_mode=w.SCALE_GROUP_F16))
+                nbytes += N * K // 2 + sc.numel() * 2 + M * K * 2 + M * N * 2
+
+        def run_all(stream):
+            for c in calls:
+                c(0, stream)
+
+        stream = torch.cuda.current_stream().cuda_stream
+        ms_eager = time_steps(lambda i: run_all(stream), steps, 3)
+        g = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            run_all(cap.cuda_stream)  # warm the capture stream
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=cap):
+                run_all(cap.cuda_stream)
+        torch.cuda.current_stream().wait_stream(cap)
+        ms_graph = time_steps(lambda i: g.replay(), steps, 3)
+        rows.append({"M": M, "linears": len(calls), "us_eager": round(ms_eager * 1e3, 1),
+                     "us_graph": round(ms_graph * 1e3, 1), "GB/s_graph": round(nbytes / (ms_graph * 1e-3) / 1e9, 1),
+                     "frac_hbm_graph": round(nbytes / (ms_graph * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "algorithmic_bytes": nbytes})
+        del calls, g
+    del weights, base
+    torch.cuda.empty_cache()
+    return {"workload": f"{layers}-layer backbone linears per decode/verify step (QKV, O, gate+up, down; "
+                        "group-128 fp16 scales)", "rows": rows}
+
+
 def measure_ceilings():
     """Measured HBM-read and INT8-MFMA ceilings (libw4a8_ceiling.so): a plain
     16-byte streaming read of 1 GiB, and independent 32x32x32 int8 MFMA
@@ -376,7 +431,8 @@ def main():
     if args.sweep_only:
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
         print(json.dumps({"sweep": {"down_verify": bench_down_verify(ss, sw),
-                                    "layer_group": bench_layer_group(ss, sw)}}), flush=True)
+                                    "layer_group": bench_layer_group(ss, sw),
+                                    "stack": bench_stack(max(10, args.steps // 50))}}), flush=True)
         return
     d, ms, algo_bytes, ms_gemm, gemm_bytes = bench_gate_up(args.steps, args.warmup)
     gbs = algo_bytes / (ms * 1e-3) / 1e9
@@ -427,7 +483,8 @@ def main():
     out["ceilings"] = measure_ceilings()
     if not args.no_sweep:
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
-        out["sweep"] = {"down_verify": bench_down_verify(ss, sw), "layer_group": bench_layer_group(ss, sw)}
+        out["sweep"] = {"down_verify": bench_down_verify(ss, sw), "layer_group": bench_layer_group(ss, sw),
+                        "stack": bench_stack(max(10, args.steps // 50))}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(d, algo_bytes)
     print(json.dumps(out), flush=True)

@@ -14,7 +14,6 @@ LargeMKernelFn channel_kernel(int cfg) {
     case 0: return menu_kernel<0, false>();
     case 1: return menu_kernel<1, false>();
     case 2: return menu_kernel<2, false>();
-    case 3: return menu_kernel<3, false>();
     default: return nullptr;
   }
 }

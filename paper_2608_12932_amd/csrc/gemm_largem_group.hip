@@ -14,7 +14,6 @@ LargeMKernelFn largem_group_kernel(int cfg) {
   switch (cfg) {
     case 1: return menu_kernel<1, true>();
     case 2: return menu_kernel<2, true>();
-    case 3: return menu_kernel<3, true>();
     default: return nullptr;  // 128 x 192 does not fit the group accumulators
   }
 }

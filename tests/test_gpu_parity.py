@@ -136,9 +136,9 @@ def test_large_m_per_channel(M, K, N, codes):
 
 # ------------------------------------------------------------ linear, group scales
 
-# small-M kernels, then large-M tiles 64x64 (two accumulator sets) and
-# 128x128 / 64x96 (one set, rescale wrapping into the next step), with
-# ragged row and column tails and odd step counts
+# small-M kernels, then the large-M tiles 64x64 (two accumulator sets) and
+# 128x128 (one set, rescale wrapping into the next step), with ragged row
+# and column tails and odd step counts
 @pytest.mark.parametrize("M,K,N", [(1, 4096, 256), (16, 1024, 384), (5, 12288, 128), (48, 512, 64),
                                    (100, 1024, 192), (256, 1024, 1024), (513, 256, 80),
                                    (1000, 384, 4080), (1500, 256, 2032), (1000, 640, 6128)])

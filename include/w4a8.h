@@ -119,8 +119,9 @@ w4a8_status w4a8_quantize_act(const uint16_t* x, int64_t M, int64_t K, int8_t* x
 
 /*
  * Bytes of device workspace w4a8_linear needs for this problem (0 if none).
- * The workspace holds split-K partial sums and arrival counters (and, for
- * large M with bf16 input, the int8 codes and scales).  The caller must
+ * The workspace holds split-K partial sums and arrival counters (and, when
+ * bf16 input is quantized by its own kernel, the int8 codes and scales).
+ * The caller must
  * zero-fill a workspace once before its first use; every call leaves its
  * counters at zero again, so the same workspace can be reused by later
  * calls on the same stream.  Returns 0 as well for invalid shapes.
@@ -143,6 +144,8 @@ size_t w4a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mo
  *                  aligned, zero-filled before its first use (may be NULL if
  *                  the size is 0)
  * Does not synchronize.  Deterministic: the same inputs give the same bits.
+ * Enqueues kernels only (no allocation, memory set or copy), so a call can
+ * be captured into a HIP graph on `stream` and replayed.
  */
 w4a8_status w4a8_linear(const void* x, int in_kind, const float* x_scale, int64_t M, int64_t K,
                         const uint8_t* w_packed, const void* w_scale, int scale_mode, int64_t N,

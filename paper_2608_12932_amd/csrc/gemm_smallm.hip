@@ -12,15 +12,12 @@
 //   - the partial sums of the 8 waves are reduced through LDS, and K splits
 //     across workgroups (S > 1) meet in a workspace, where the last arriving
 //     workgroup of a column group sums them in split order and finishes;
-//   - with bf16 input the per-token quantize is fused in front, in one of two
-//     ways.  Register mode (one K split, at most 4 blocks per wave): each lane
-//     loads exactly the bf16 values its own A fragments need, the row maxima
-//     meet through two shuffles and one LDS atomic per row, and each lane
-//     quantizes its values in registers; the 8 waves read the activations
-//     once per workgroup.  LDS mode (longer K or several splits): every
-//     workgroup reads the whole token rows for the absmax and quantizes its
-//     own split into LDS, which the waves then read.  In both, the weight
-//     stream is already in flight while the codes are made.
+//   - with bf16 input and a narrow column group over a long K, the
+//     per-token quantize is fused in front: every workgroup reads the whole
+//     token rows for the absmax (shuffles and one LDS atomic per row) and
+//     quantizes its own split into LDS, issuing the weight stages in between,
+//     and the waves then read the codes from LDS.  Otherwise a separate
+//     quantize kernel has written the codes, which the waves load per stage.
 // The epilogue applies the per-token and per-channel (or per-group) scales.
 #include <cmath>
 #include <cstdio>
@@ -115,7 +112,8 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   const int kb_begin = split * a.kbs;
   const int kb_end = min(KB, kb_begin + a.kbs);
   const int nkb = kb_end - kb_begin;
-  // Uniform trip count: stages past the end of the split load zeros.
+  // Uniform trip count (blocks per wave, rounded up): a wave's blocks past
+  // the split read zeros; whole stages past it are skipped.
   const int iters = (nkb + kWaves - 1) / kWaves;
   const int r16 = lane & 15, g4 = lane >> 4;
   const int ldq = nkb * 128 + 16;  // fused: LDS row stride of the codes

@@ -37,7 +37,7 @@ struct SmallMPlan {
   int MT, NT;            // 16-row tiles, 16-column tiles per workgroup
   int S;                 // K splits over workgroups
   bool fused;            // quantize inside the GEMM
-  int qmode;             // 0 int8 codes in, 1 fused via LDS, 2 fused in registers
+  int qmode;             // 0 int8 codes in, 1 quantize fused, codes made in LDS
   bool group;            // group-wise scales
   int groups;            // workgroups along N
   int tpr;               // fused quantize: threads per token row

@@ -30,7 +30,6 @@ struct SmallMArgs {
   int M, N, K, KB;
   int S, kbs;            // K splits and 128-k blocks per split
   int tpr;               // fused quantize: threads per token row
-  bool exact;            // every wave's block count is a multiple of the stage depth
   int out_kind;
 };
 struct SmallMPlan {

@@ -43,8 +43,8 @@ METRIC = "W4A8 linear: HBM GB/s at M=16, INT8 TOPS at M=1024 (% of roofline)"
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 INT8_PEAK_TOPS = 5000.0      # MI355X dense INT8 MFMA (5.0 POPS)
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ["device.h", "gemm_smallm.hip", "largem_kernel.h", "gemm_largem.hip", "gemm_largem_group.hip",
-                  "quantize.hip", "api.cpp"]
+KERNEL_SOURCES = ["device.h", "kernels.h", "gemm_smallm.hip", "largem_kernel.h", "gemm_largem.hip",
+                  "gemm_largem_group.hip", "quantize.hip", "api.cpp"]
 
 
 def kernel_source_hash() -> str:

@@ -272,8 +272,15 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
     }
 
   // Stage s of the block at base: compute block i = base + s from slot s.
+  // Group mode issues every tile's two MFMAs first and then the rescales,
+  // so the MFMAs run back to back and the rescales of one tile do not wait
+  // on the MFMA latency of the next.  Its partial sums are kept 16x too
+  // large (the unpacked weights' factor, taken out exactly in the
+  // epilogue), so the fp16 scale feeds the FMA directly: one
+  // v_fma_mix_f32 per value, with no conversion or multiply of the scale.
   auto compute_stage = [&](int s, int i) {
     v4i alo[MT], ahi[MT];
+    v4i pg[GROUP ? MT : 1][GROUP ? NT : 1];
     if constexpr (QM == kQLds) {
       // Rows past M and stages past the split read clamped LDS addresses:
       // their weights are zero, and rows past M are never stored.
@@ -295,15 +302,22 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         if constexpr (GROUP) {
-          v4i p = mfma16(alo[mt], blo, zero4);
-          p = mfma16(ahi[mt], bhi, p);
-          const float sg = f16_to_f32(sgb[s][t]) * 0.0625f;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) facc[mt][t][r] = __fmaf_rn((float)p[r], sg, facc[mt][t][r]);
+          pg[mt][t] = mfma16(alo[mt], blo, zero4);
+          pg[mt][t] = mfma16(ahi[mt], bhi, pg[mt][t]);
         } else {
           acc[mt][t] = mfma16(alo[mt], blo, acc[mt][t]);
           acc[mt][t] = mfma16(ahi[mt], bhi, acc[mt][t]);
         }
+      }
+    }
+    if constexpr (GROUP) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const float sg = f16_to_f32(sgb[s][t]);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) facc[mt][t][r] = __fmaf_rn((float)pg[mt][t][r], sg, facc[mt][t][r]);
       }
     }
   };
@@ -365,6 +379,7 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
       float v = 0.0f;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) v += __uint_as_float(red[((w * MT + mt) * NT + t) * 256 + src]);
+      v *= 0.0625f;  // every partial and sum above is 16x the true one: exact barring underflow
       if (a.S == 1)
         emit.group(row, n, v, sxp[q]);
       else
@@ -419,13 +434,16 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
 typedef void (*SmallMKernel)(const SmallMArgs);
 
 // MT * NT is capped at 12 (kMaxTilesPerWave): beyond it the accumulators
-// and in-flight operands no longer fit in 256 registers.
+// and in-flight operands no longer fit in 256 registers.  Group kernels
+// have no EXACT form (the planner never asks for one).
 template <int MT, int NT, bool GROUP, int QM>
 SmallMKernel instance(bool exact) {
-  if constexpr (MT * NT <= kMaxTilesPerWave && (QM == kQNone || MT == 1))
-    return exact ? smallm<MT, NT, GROUP, QM, true> : smallm<MT, NT, GROUP, QM, false>;
-  else
+  if constexpr (MT * NT > kMaxTilesPerWave || (QM != kQNone && MT != 1))
     return nullptr;
+  else if constexpr (GROUP)
+    return exact ? nullptr : smallm<MT, NT, GROUP, QM, false>;
+  else
+    return exact ? smallm<MT, NT, GROUP, QM, true> : smallm<MT, NT, GROUP, QM, false>;
 }
 
 template <int MT, bool GROUP, int QM>

@@ -34,7 +34,10 @@ def quant_gpu(x_bits):
 
 @pytest.mark.parametrize("M,K,seed", [(4, 256, 1), (16, 4096, 2), (16, 12288, 3), (1024, 4096, 4),
                                       (3, 128, 5), (17, 640, 6), (1000, 384, 7), (2, 65536, 8),
-                                      (65, 65536, 9), (301, 12288, 10), (66, 4224, 11)])
+                                      (65, 65536, 9), (301, 12288, 10), (66, 4224, 11),
+                                      # every threads-per-row / chunks-per-thread choice of the launcher
+                                      (200, 1024, 12), (130, 2048, 13), (8, 8192, 14), (100, 8192, 15),
+                                      (5, 2048, 16)])
 def test_quantize_bit_exact(M, K, seed):
     print(f"[case] quantize M={M} K={K} seed={seed}", flush=True)
     x = I.activations(M, K, seed)

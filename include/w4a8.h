@@ -161,6 +161,42 @@ w4a8_status w4a8_linear(const void* x, int in_kind, const float* x_scale, int64_
 const char* w4a8_linear_describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind,
                                  int out_kind);
 
+/*
+ * The fused gate+up projection with its gated activation merged into the
+ * GEMM's epilogue.  FlashDrive, Sec. 3.5 ("Kernel Fusion"), runs the MLP's
+ * gate and up projections as one GEMM and merges the element-wise
+ * operations that follow into the kernels; the paper does not name the
+ * activation, and this library takes SiLU (a reading: the usual gated-MLP
+ * activation):
+ *     y[m][f] = silu(g[m][f]) * u[m][f],   silu(g) = g / (1 + e^-g),
+ * where g[m][f] and u[m][f] are the fp32 values w4a8_linear computes for
+ * output columns f (gate) and N/2 + f (up) of the same call, before their
+ * bf16 rounding.  silu and the product are evaluated in fp32 (e^-g with the
+ * fast exponential), the result is rounded once to the output type.
+ *   - W [N][K] holds the gate rows [0, N/2) followed by the up rows
+ *     [N/2, N), packed by w4a8_pack_weights as one weight; w_scale covers
+ *     all N columns in that order (fp32 [N] or fp16 [K/128][N]).
+ *   - y is [M][N/2] of out_kind, W4A8_OUT_BF16 or W4A8_OUT_F32.
+ *   - N % 32 == 0 (whole 16-column tiles in each half); other arguments and
+ *     the workspace as for w4a8_linear, with its own size query below.
+ *   - The decode / draft-block verification path only: 1 <= M <= 64
+ *     (W4A8_EUNSUPPORTED above; M == 0 is a no-op).  W4A8_OUT_I32_ACC and
+ *     N % 32 != 0 are W4A8_EINVAL.
+ * Does not synchronize; enqueues kernels only (graph-capturable), like
+ * w4a8_linear.
+ */
+w4a8_status w4a8_linear_swiglu(const void* x, int in_kind, const float* x_scale, int64_t M, int64_t K,
+                               const uint8_t* w_packed, const void* w_scale, int scale_mode, int64_t N,
+                               void* y, int out_kind, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+
+/* Workspace bytes w4a8_linear_swiglu needs (0 if none, and 0 for shapes it
+ * rejects); the same zero-fill-once contract as w4a8_linear's workspace. */
+size_t w4a8_linear_swiglu_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind);
+
+/* The kernels w4a8_linear_swiglu would use, as w4a8_linear_describe. */
+const char* w4a8_linear_swiglu_describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind);
+
 #ifdef __cplusplus
 }
 #endif

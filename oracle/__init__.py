@@ -2,9 +2,10 @@
 
 TEST INFRASTRUCTURE ONLY: imported by tests/, by the package smoke check and
 by the CPU-baseline leg of bench.py, never by the product path.  It shares no
-code with the HIP sources.  Every function follows FlashDrive Sec. 3.4
-(4-bit weights, 8-bit activations, integer contraction) with the readings
-stated in oracle.c's header.
+code with the HIP sources.  The linear-layer functions follow FlashDrive
+Sec. 3.4 (4-bit weights, 8-bit activations, integer contraction) with the
+readings stated in oracle.c's header; silu_mul / gated follow Sec. 3.5
+(Kernel Fusion) with the SiLU reading stated in silu_mul.
 """
 from __future__ import annotations
 
@@ -129,3 +130,31 @@ def linear(x_bits, w, s_w=None, s_g=None, nthreads=1):
                              _ptr(out["y"]), _ptr(out["y64"]), _ptr(out["bound"]))
     _check(rc, "linear")
     return out
+
+
+def silu_mul(g, u):
+    """silu(g) * u in fp64, with silu(g) = g / (1 + e^-g).
+
+    The gated activation merged into the fused gate+up projection.
+    FlashDrive Sec. 3.5 (Kernel Fusion) fuses the MLP's gate and up
+    projections into one GEMM and merges the element-wise operations after
+    it, without naming the activation; SiLU gating is this oracle's reading.
+    """
+    g = np.asarray(g, np.float64)
+    u = np.asarray(u, np.float64)
+    with np.errstate(over="ignore"):
+        return g / (1.0 + np.exp(-g)) * u
+
+
+def gated(out):
+    """The gated output of a linear() / linear_q() result whose weight holds
+    the gate rows [0, N/2) followed by the up rows [N/2, N).
+
+    Returns y64 (silu_mul of the fp64 gate and up values), y_of32 (silu_mul
+    of their fp32 values y32, the values the per-channel kernel holds before
+    its fp32 activation), and the halves' fp64 values and error bounds."""
+    F = out["y64"].shape[1] // 2
+    g64, u64 = out["y64"][:, :F], out["y64"][:, F:]
+    g32, u32 = out["y32"][:, :F], out["y32"][:, F:]
+    return dict(y64=silu_mul(g64, u64), y_of32=silu_mul(g32, u32), g64=g64, u64=u64,
+                g_bound=out["bound"][:, :F], u_bound=out["bound"][:, F:])

@@ -25,7 +25,8 @@ GROUP_SIZE = 128
 
 EXPORTS = ("w4a8_status_string", "w4a8_packed_weight_bytes", "w4a8_pack_weights",
            "w4a8_quantize_act", "w4a8_linear_workspace_bytes", "w4a8_linear",
-           "w4a8_linear_describe")
+           "w4a8_linear_describe", "w4a8_linear_swiglu", "w4a8_linear_swiglu_workspace_bytes",
+           "w4a8_linear_swiglu_describe")
 
 _OUT_DTYPE = {OUT_BF16: torch.bfloat16, OUT_F32: torch.float32, OUT_I32_ACC: torch.int32}
 
@@ -62,6 +63,12 @@ def lib() -> ctypes.CDLL:
         L.w4a8_linear.restype = I
         L.w4a8_linear_describe.argtypes = [I64, I64, I64, I, I, I]
         L.w4a8_linear_describe.restype = ctypes.c_char_p
+        L.w4a8_linear_swiglu_workspace_bytes.argtypes = [I64, I64, I64, I, I]
+        L.w4a8_linear_swiglu_workspace_bytes.restype = SZ
+        L.w4a8_linear_swiglu.argtypes = [P, I, P, I64, I64, P, P, I, I64, P, I, P, SZ, P]
+        L.w4a8_linear_swiglu.restype = I
+        L.w4a8_linear_swiglu_describe.argtypes = [I64, I64, I64, I, I]
+        L.w4a8_linear_swiglu_describe.restype = ctypes.c_char_p
         _lib = L
     return _lib
 
@@ -145,16 +152,8 @@ class Workspace:
         return self.buf
 
 
-def w4a8_linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor | None, N: int, *,
-                x_scale: torch.Tensor | None = None, scale_mode: int = SCALE_CHANNEL_F32,
-                out_kind: int = OUT_BF16, out: torch.Tensor | None = None,
-                workspace: Workspace | torch.Tensor | None = None, stream=None) -> torch.Tensor:
-    """y[M][N] = dequant(quant8(x) . W^T).
-
-    x is bf16 [M][K] (quantized inside the call) or int8 codes [M][K] with
-    x_scale fp32 [M].  w_scale is fp32 [N] (SCALE_CHANNEL_F32) or fp16
-    [K/128][N] (SCALE_GROUP_F16).  Returns bf16, fp32 or int32 [M][N].
-    """
+def _linear_call(entry: str, x, w_packed, w_scale, N, out_cols, x_scale, scale_mode, out_kind, out,
+                 workspace, stream):
     M, K = x.shape
     if x.dtype == torch.bfloat16:
         in_kind = IN_BF16
@@ -173,9 +172,11 @@ def w4a8_linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor |
     else:
         ws_ptr = _dev(w_scale, "w_scale", torch.float32 if scale_mode == SCALE_CHANNEL_F32 else torch.float16)
     if out is None:
-        out = torch.empty((M, N), dtype=_OUT_DTYPE[out_kind], device=x.device)
+        out = torch.empty((M, out_cols), dtype=_OUT_DTYPE[out_kind], device=x.device)
+    elif tuple(out.shape) != (M, out_cols):
+        raise ValueError(f"out must be [{M}][{out_cols}]")
     y_ptr = _dev(out, "out", _OUT_DTYPE[out_kind])
-    need = w4a8_linear_workspace_bytes(M, N, K, scale_mode, in_kind)
+    need = int(getattr(lib(), entry + "_workspace_bytes")(M, N, K, scale_mode, in_kind))
     if need == 0:
         wk_ptr, wk_bytes = None, 0
     else:
@@ -183,7 +184,44 @@ def w4a8_linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor |
             workspace = torch.zeros(need, dtype=torch.uint8, device=x.device)
         buf = workspace.get(need) if isinstance(workspace, Workspace) else workspace
         wk_ptr, wk_bytes = _dev(buf, "workspace", torch.uint8), buf.numel()
-    rc = lib().w4a8_linear(x_ptr, in_kind, xs_ptr, M, K, wp_ptr, ws_ptr, scale_mode, N, y_ptr,
-                           out_kind, wk_ptr, wk_bytes, _stream(stream))
-    _check(rc, "w4a8_linear")
+    rc = getattr(lib(), entry)(x_ptr, in_kind, xs_ptr, M, K, wp_ptr, ws_ptr, scale_mode, N, y_ptr,
+                               out_kind, wk_ptr, wk_bytes, _stream(stream))
+    _check(rc, entry)
     return out
+
+
+def w4a8_linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor | None, N: int, *,
+                x_scale: torch.Tensor | None = None, scale_mode: int = SCALE_CHANNEL_F32,
+                out_kind: int = OUT_BF16, out: torch.Tensor | None = None,
+                workspace: Workspace | torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """y[M][N] = dequant(quant8(x) . W^T).
+
+    x is bf16 [M][K] (quantized inside the call) or int8 codes [M][K] with
+    x_scale fp32 [M].  w_scale is fp32 [N] (SCALE_CHANNEL_F32) or fp16
+    [K/128][N] (SCALE_GROUP_F16).  Returns bf16, fp32 or int32 [M][N].
+    """
+    return _linear_call("w4a8_linear", x, w_packed, w_scale, N, N, x_scale, scale_mode, out_kind, out,
+                        workspace, stream)
+
+
+def w4a8_linear_swiglu_workspace_bytes(M: int, N: int, K: int, scale_mode: int = SCALE_CHANNEL_F32,
+                                       in_kind: int = IN_BF16) -> int:
+    return int(lib().w4a8_linear_swiglu_workspace_bytes(M, N, K, scale_mode, in_kind))
+
+
+def w4a8_linear_swiglu_describe(M: int, N: int, K: int, scale_mode: int = SCALE_CHANNEL_F32,
+                                in_kind: int = IN_BF16) -> str:
+    return lib().w4a8_linear_swiglu_describe(M, N, K, scale_mode, in_kind).decode()
+
+
+def w4a8_linear_swiglu(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor | None, N: int, *,
+                       x_scale: torch.Tensor | None = None, scale_mode: int = SCALE_CHANNEL_F32,
+                       out_kind: int = OUT_BF16, out: torch.Tensor | None = None,
+                       workspace: Workspace | torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Fused gate+up projection with its gated activation, M <= 64:
+    y[M][N/2] = silu(g) * u, where g and u are the fp32 outputs of
+    w4a8_linear over weight rows [0, N/2) (gate) and [N/2, N) (up) of the
+    same packed weight.  Arguments as for w4a8_linear; out_kind bf16 or fp32.
+    """
+    return _linear_call("w4a8_linear_swiglu", x, w_packed, w_scale, N, N // 2, x_scale, scale_mode, out_kind,
+                        out, workspace, stream)

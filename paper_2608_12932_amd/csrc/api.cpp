@@ -33,12 +33,13 @@ struct Plan {
   size_t off_counters = 0, off_partial = 0, off_xq = 0, off_sx = 0, total = 0;
 };
 
-Plan make_plan(int64_t M, int64_t N, int64_t K, bool group, bool bf16_in) {
+// Gated plans (swiglu) exist only for M <= kSmallMMaxM.
+Plan make_plan(int64_t M, int64_t N, int64_t K, bool group, bool bf16_in, bool swiglu = false) {
   Plan p;
   p.small_m = M <= kSmallMMaxM;
   size_t off = 0;
   if (p.small_m) {
-    p.sm = plan_smallm((int)M, (int)N, (int)K, group, bf16_in);
+    p.sm = plan_smallm((int)M, (int)N, (int)K, group, bf16_in, swiglu);
     p.separate_quant = bf16_in && !p.sm.fused;
     if (p.sm.S > 1) {
       p.off_counters = off;
@@ -61,6 +62,115 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, bool group, bool bf16_in) {
 }
 
 std::mutex g_pack_mutex;
+
+bool valid_modes(int scale_mode, int in_kind) {
+  return (scale_mode == W4A8_SCALE_CHANNEL_F32 || scale_mode == W4A8_SCALE_GROUP_F16) &&
+         (in_kind == W4A8_IN_BF16 || in_kind == W4A8_IN_I8);
+}
+
+// Shapes the gated entry points take: an even number of 16-column tiles
+// (gate and up halves of whole tiles) and the small-M path.
+bool gated_shape(int64_t M, int64_t N) { return N % 32 == 0 && M <= kSmallMMaxM; }
+
+// Both linear entry points after their own checks: the rest of the
+// validation, the plan, and the launches.
+w4a8_status run_linear(const void* x, int in_kind, const float* x_scale, int64_t M, int64_t K,
+                       const uint8_t* w_packed, const void* w_scale, int scale_mode, int64_t N, void* y,
+                       int out_kind, void* workspace, size_t workspace_bytes, hipStream_t stream,
+                       bool swiglu) {
+  if (M < 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return W4A8_EINVAL;
+  if (!valid_modes(scale_mode, in_kind)) return W4A8_EINVAL;
+  if (out_kind != W4A8_OUT_BF16 && out_kind != W4A8_OUT_F32 && out_kind != W4A8_OUT_I32_ACC)
+    return W4A8_EINVAL;
+  if (swiglu && (out_kind == W4A8_OUT_I32_ACC || N % 32)) return W4A8_EINVAL;
+  if (M == 0) return W4A8_OK;
+  if (swiglu && M > kSmallMMaxM) return W4A8_EUNSUPPORTED;
+  // 32-bit buffer offsets: the group-scale array (N*K/64 bytes) stays below 2 GiB
+  if ((uint64_t)N * (uint64_t)K >= (uint64_t(1) << 37)) return W4A8_EUNSUPPORTED;
+  if (!x || !aligned(x, 16) || !w_packed || !aligned(w_packed, 16) || !y || !aligned(y, 16))
+    return W4A8_EINVAL;
+  if (in_kind == W4A8_IN_I8 && (!x_scale || !aligned(x_scale, 4))) return W4A8_EINVAL;
+  if (out_kind != W4A8_OUT_I32_ACC &&
+      (!w_scale || !aligned(w_scale, scale_mode == W4A8_SCALE_CHANNEL_F32 ? 4 : 2)))
+    return W4A8_EINVAL;
+
+  // The integer accumulator does not depend on the scales, so the raw
+  // accumulator output always takes the per-channel kernels.
+  const bool group = scale_mode == W4A8_SCALE_GROUP_F16 && out_kind != W4A8_OUT_I32_ACC;
+  const bool bf16_in = in_kind == W4A8_IN_BF16;
+  const Plan p = make_plan(M, N, K, group, bf16_in, swiglu);
+  if (workspace_bytes < p.total) return W4A8_EINVAL;
+  if (p.total && (!workspace || !aligned(workspace, 256))) return W4A8_EINVAL;
+
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  const void* xin = x;
+  const float* sx = x_scale;
+  if (p.separate_quant) {
+    int8_t* xq = reinterpret_cast<int8_t*>(ws + p.off_xq);
+    float* s = reinterpret_cast<float*>(ws + p.off_sx);
+    if (launch_quantize(static_cast<const uint16_t*>(x), (int)M, (int)K, xq, s, stream) != hipSuccess)
+      return W4A8_EHIP;
+    xin = xq;
+    sx = s;
+  }
+
+  hipError_t e;
+  if (p.small_m) {
+    SmallMArgs a{};
+    a.x = xin;
+    a.x_scale = sx;
+    a.wp = w_packed;
+    a.w_scale = w_scale;
+    a.y = y;
+    a.partial = p.sm.S > 1 ? ws + p.off_partial : nullptr;
+    a.counters = p.sm.S > 1 ? reinterpret_cast<unsigned*>(ws + p.off_counters) : nullptr;
+    a.M = (int)M;
+    a.N = (int)N;
+    a.K = (int)K;
+    a.KB = (int)(K / W4A8_GROUP_SIZE);
+    a.S = p.sm.S;
+    a.kbs = (a.KB + p.sm.S - 1) / p.sm.S;
+    a.tpr = p.sm.tpr;
+    a.out_kind = out_kind;
+    a.F = swiglu ? (int)(N / 2) : 0;
+    e = launch_smallm(p.sm, a, stream);
+  } else {
+    LargeMArgs a{};
+    a.xq = static_cast<const int8_t*>(xin);
+    a.x_scale = sx;
+    a.wp = w_packed;
+    a.w_scale = w_scale;
+    a.y = y;
+    a.M = (int)M;
+    a.N = (int)N;
+    a.K = (int)K;
+    a.KB = (int)(K / W4A8_GROUP_SIZE);
+    a.out_kind = out_kind;
+    a.tiles_m = p.lm.tiles_m;
+    a.tiles_n = p.lm.tiles_n;
+    a.xcd_remap = (p.lm.tiles_m * p.lm.tiles_n) % 8 == 0;
+    e = launch_largem(p.lm, a, stream);
+  }
+  return e == hipSuccess ? W4A8_OK : W4A8_EHIP;
+}
+
+size_t workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind, bool swiglu) {
+  if (M < 0 || M > W4A8_M_MAX || !valid_nk(N, K) || !valid_modes(scale_mode, in_kind)) return 0;
+  if (M == 0 || (uint64_t)N * (uint64_t)K >= (uint64_t(1) << 37)) return 0;
+  if (swiglu && !gated_shape(M, N)) return 0;
+  return make_plan(M, N, K, scale_mode == W4A8_SCALE_GROUP_F16, in_kind == W4A8_IN_BF16, swiglu).total;
+}
+
+const char* describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind, int out_kind, bool swiglu) {
+  static thread_local char buf[256];
+  if (M <= 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return "invalid shape";
+  if (swiglu && !gated_shape(M, N)) return "invalid shape";
+  const bool group = scale_mode == W4A8_SCALE_GROUP_F16 && out_kind != W4A8_OUT_I32_ACC;
+  const Plan p = make_plan(M, N, K, group, in_kind == W4A8_IN_BF16, swiglu);
+  snprintf(buf, sizeof buf, "%s%s workspace=%zu", p.separate_quant ? "quantize_rows + " : "",
+           p.small_m ? smallm_kernel_name(p.sm) : largem_kernel_name(p.lm), p.total);
+  return buf;
+}
 
 }  // namespace
 
@@ -107,113 +217,36 @@ w4a8_status w4a8_quantize_act(const uint16_t* x, int64_t M, int64_t K, int8_t* x
 }
 
 size_t w4a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind) {
-  if (M < 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return 0;
-  if (scale_mode != W4A8_SCALE_CHANNEL_F32 && scale_mode != W4A8_SCALE_GROUP_F16) return 0;
-  if (in_kind != W4A8_IN_BF16 && in_kind != W4A8_IN_I8) return 0;
-  if (M == 0 || (uint64_t)N * (uint64_t)K >= (uint64_t(1) << 37)) return 0;
-  return make_plan(M, N, K, scale_mode == W4A8_SCALE_GROUP_F16, in_kind == W4A8_IN_BF16).total;
+  return workspace_bytes(M, N, K, scale_mode, in_kind, false);
 }
 
 const char* w4a8_linear_describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind,
                                  int out_kind) {
-  static thread_local char buf[256];
-  if (M <= 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return "invalid shape";
-  const bool group = scale_mode == W4A8_SCALE_GROUP_F16 && out_kind != W4A8_OUT_I32_ACC;
-  const Plan p = make_plan(M, N, K, group, in_kind == W4A8_IN_BF16);
-  if (p.small_m) {
-    SmallMPlan sm = p.sm;
-    sm.group = group;
-    snprintf(buf, sizeof buf, "%s%s workspace=%zu", p.separate_quant ? "quantize_rows + " : "",
-             smallm_kernel_name(sm), p.total);
-  } else {
-    snprintf(buf, sizeof buf, "%s%s workspace=%zu", p.separate_quant ? "quantize_rows + " : "",
-             largem_kernel_name(p.lm), p.total);
-  }
-  return buf;
+  return describe(M, N, K, scale_mode, in_kind, out_kind, false);
 }
 
 w4a8_status w4a8_linear(const void* x, int in_kind, const float* x_scale, int64_t M, int64_t K,
                         const uint8_t* w_packed, const void* w_scale, int scale_mode, int64_t N,
                         void* y, int out_kind, void* workspace, size_t workspace_bytes,
                         hipStream_t stream) {
-  if (M < 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return W4A8_EINVAL;
-  if (in_kind != W4A8_IN_BF16 && in_kind != W4A8_IN_I8) return W4A8_EINVAL;
-  if (scale_mode != W4A8_SCALE_CHANNEL_F32 && scale_mode != W4A8_SCALE_GROUP_F16) return W4A8_EINVAL;
-  if (out_kind != W4A8_OUT_BF16 && out_kind != W4A8_OUT_F32 && out_kind != W4A8_OUT_I32_ACC)
-    return W4A8_EINVAL;
-  if (M == 0) return W4A8_OK;
-  // 32-bit buffer offsets: the group-scale array (N*K/64 bytes) stays below 2 GiB
-  if ((uint64_t)N * (uint64_t)K >= (uint64_t(1) << 37)) return W4A8_EUNSUPPORTED;
-  if (!x || !aligned(x, 16) || !w_packed || !aligned(w_packed, 16) || !y || !aligned(y, 16))
-    return W4A8_EINVAL;
-  if (in_kind == W4A8_IN_I8 && (!x_scale || !aligned(x_scale, 4))) return W4A8_EINVAL;
-  if (out_kind != W4A8_OUT_I32_ACC &&
-      (!w_scale || !aligned(w_scale, scale_mode == W4A8_SCALE_CHANNEL_F32 ? 4 : 2)))
-    return W4A8_EINVAL;
+  return run_linear(x, in_kind, x_scale, M, K, w_packed, w_scale, scale_mode, N, y, out_kind, workspace,
+                    workspace_bytes, stream, false);
+}
 
-  // The integer accumulator does not depend on the scales, so the raw
-  // accumulator output always takes the per-channel kernels.
-  const bool group = scale_mode == W4A8_SCALE_GROUP_F16 && out_kind != W4A8_OUT_I32_ACC;
-  const bool bf16_in = in_kind == W4A8_IN_BF16;
-  const Plan p = make_plan(M, N, K, group, bf16_in);
-  if (workspace_bytes < p.total) return W4A8_EINVAL;
-  if (p.total && (!workspace || !aligned(workspace, 256))) return W4A8_EINVAL;
+size_t w4a8_linear_swiglu_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind) {
+  return workspace_bytes(M, N, K, scale_mode, in_kind, true);
+}
 
-  uint8_t* ws = static_cast<uint8_t*>(workspace);
-  const void* xin = x;
-  const float* sx = x_scale;
-  if (p.separate_quant) {
-    int8_t* xq = reinterpret_cast<int8_t*>(ws + p.off_xq);
-    float* s = reinterpret_cast<float*>(ws + p.off_sx);
-    if (launch_quantize(static_cast<const uint16_t*>(x), (int)M, (int)K, xq, s, stream) != hipSuccess)
-      return W4A8_EHIP;
-    xin = xq;
-    sx = s;
-  }
+const char* w4a8_linear_swiglu_describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind) {
+  return describe(M, N, K, scale_mode, in_kind, W4A8_OUT_BF16, true);
+}
 
-  hipError_t e;
-  if (p.small_m) {
-    SmallMPlan sm = p.sm;
-    sm.group = group;
-    if (!bf16_in) {
-      sm.fused = false;
-      sm.qmode = 0;
-    }
-    SmallMArgs a{};
-    a.x = xin;
-    a.x_scale = sx;
-    a.wp = w_packed;
-    a.w_scale = w_scale;
-    a.y = y;
-    a.partial = sm.S > 1 ? ws + p.off_partial : nullptr;
-    a.counters = sm.S > 1 ? reinterpret_cast<unsigned*>(ws + p.off_counters) : nullptr;
-    a.M = (int)M;
-    a.N = (int)N;
-    a.K = (int)K;
-    a.KB = (int)(K / W4A8_GROUP_SIZE);
-    a.S = sm.S;
-    a.kbs = (a.KB + sm.S - 1) / sm.S;
-    a.tpr = sm.tpr;
-    a.out_kind = out_kind;
-    e = launch_smallm(sm, a, stream);
-  } else {
-    LargeMArgs a{};
-    a.xq = static_cast<const int8_t*>(xin);
-    a.x_scale = sx;
-    a.wp = w_packed;
-    a.w_scale = w_scale;
-    a.y = y;
-    a.M = (int)M;
-    a.N = (int)N;
-    a.K = (int)K;
-    a.KB = (int)(K / W4A8_GROUP_SIZE);
-    a.out_kind = out_kind;
-    a.tiles_m = p.lm.tiles_m;
-    a.tiles_n = p.lm.tiles_n;
-    a.xcd_remap = (p.lm.tiles_m * p.lm.tiles_n) % 8 == 0;
-    e = launch_largem(p.lm, a, stream);
-  }
-  return e == hipSuccess ? W4A8_OK : W4A8_EHIP;
+w4a8_status w4a8_linear_swiglu(const void* x, int in_kind, const float* x_scale, int64_t M, int64_t K,
+                               const uint8_t* w_packed, const void* w_scale, int scale_mode, int64_t N,
+                               void* y, int out_kind, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream) {
+  return run_linear(x, in_kind, x_scale, M, K, w_packed, w_scale, scale_mode, N, y, out_kind, workspace,
+                    workspace_bytes, stream, true);
 }
 
 }  // extern "C"

@@ -19,6 +19,10 @@
 //     and the waves then read the codes from LDS.  Otherwise a separate
 //     quantize kernel has written the codes, which the waves load per stage.
 // The epilogue applies the per-token and per-channel (or per-group) scales.
+// SWIGLU instances serve the fused gate+up projection with its gated
+// activation merged in (FlashDrive Sec. 3.5, Kernel Fusion): a workgroup's
+// NT tiles are NT / 2 gate tiles and the NT / 2 up tiles of the same
+// columns, and it writes silu(gate) * up, half the columns of the GEMM.
 #include <cmath>
 #include <cstdio>
 
@@ -51,9 +55,13 @@ enum QMode {
 };
 
 // Weight stages in flight per wave (used by the kernels and the planner).
-constexpr int stage_depth(int MT, int NT, int QM, bool GROUP) {
+// Gated kernels hold a second set of epilogue scales and sums: they keep
+// the base budget, less 16 registers in group mode.
+constexpr int stage_depth(int MT, int NT, int QM, bool GROUP, bool SW) {
   int per = NT * 4 + (QM == kQLds ? 0 : MT * 8);
-  int d = (QM == kQLds ? kOperandVgprsFused : !GROUP && NT <= 2 ? kOperandVgprsNarrow : kOperandVgprs) / per;
+  int budget = QM == kQLds ? kOperandVgprsFused : !GROUP && !SW && NT <= 2 ? kOperandVgprsNarrow : kOperandVgprs;
+  if (SW && GROUP) budget -= 16;
+  int d = budget / per;
   return d < 1 ? 1 : (d > 16 ? 16 : d);
 }
 
@@ -83,12 +91,28 @@ struct Emit {
     else
       static_cast<uint16_t*>(a.y)[o] = (uint16_t)f32_to_bf16(y32);
   }
+  // gated output column f from the fp32 gate and up values (the values the
+  // plain linear would round to bf16): silu(g) * u, with
+  // silu(g) = g / (1 + e^-g)
+  __device__ void gated(int row, int f, float g, float u) const {
+    const size_t o = (size_t)row * a.F + f;
+    const float y32 = __fmul_rn(__fdiv_rn(g, __fadd_rn(1.0f, __expf(-g))), u);
+    if (a.out_kind == kOutF32)
+      static_cast<float*>(a.y)[o] = y32;
+    else
+      static_cast<uint16_t*>(a.y)[o] = (uint16_t)f32_to_bf16(y32);
+  }
+  __device__ float channel_value(int v, float sx, float sw) const {
+    return __fmul_rn(__fmul_rn((float)(v >> 4), sx), sw);
+  }
 };
 
-template <int MT, int NT, bool GROUP, int QM, bool EXACT>
+template <int MT, int NT, bool GROUP, int QM, bool EXACT, bool SWIGLU>
 __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
+  static_assert(!SWIGLU || NT % 2 == 0, "gated instances pair gate and up tiles");
+  constexpr int HT = SWIGLU ? NT / 2 : NT;  // output column tiles per workgroup
   constexpr bool FUSED = QM != kQNone;
-  constexpr int D = stage_depth(MT, NT, QM, GROUP);
+  constexpr int D = stage_depth(MT, NT, QM, GROUP, SWIGLU);
   extern __shared__ __align__(16) uint8_t lds[];
   uint32_t* l_amax = reinterpret_cast<uint32_t*>(lds);
   float* l_s = reinterpret_cast<float*>(lds + 64);
@@ -109,6 +133,10 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   const int M = a.M, N = a.N, K = a.K, KB = a.KB;
   const int ntiles = N / 16;
   const int nt0 = gid * NT;
+  // Tile t < HT of this group is weight tile t0 + t; gated instances take
+  // tile t >= HT (the up half) from the same columns F / 16 tiles on.
+  const int t0 = gid * HT;
+  const int u0 = SWIGLU ? a.F / 16 + t0 : t0 + HT;
   const int kb_begin = split * a.kbs;
   const int kb_end = min(KB, kb_begin + a.kbs);
   const int nkb = kb_end - kb_begin;
@@ -120,13 +148,19 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
 
   // The NT tiles of this group are contiguous in the packed layout; tiles
   // past N fall outside the resource and read as zeros.
-  const int tiles_here = min(NT, ntiles - nt0);
-  const __amdgpu_buffer_rsrc_t wres =
-      make_rsrc(a.wp + (size_t)nt0 * KB * kBlockBytes, (uint32_t)(tiles_here * KB * kBlockBytes));
+  const int tiles_here = SWIGLU ? NT : min(NT, ntiles - nt0);
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(a.wp + (size_t)t0 * KB * kBlockBytes,
+                                                (uint32_t)((SWIGLU ? HT : tiles_here) * KB * kBlockBytes));
+  const __amdgpu_buffer_rsrc_t wres_u =
+      SWIGLU ? make_rsrc(a.wp + (size_t)u0 * KB * kBlockBytes, (uint32_t)(HT * KB * kBlockBytes)) : wres;
   const __amdgpu_buffer_rsrc_t sres =
-      GROUP ? make_rsrc(static_cast<const uint16_t*>(a.w_scale) + nt0 * 16,
-                        (uint32_t)(((size_t)KB * N - nt0 * 16) * 2))
+      GROUP ? make_rsrc(static_cast<const uint16_t*>(a.w_scale) + t0 * 16,
+                        (uint32_t)(((size_t)KB * N - t0 * 16) * 2))
             : wres;
+  const __amdgpu_buffer_rsrc_t sres_u =
+      GROUP && SWIGLU ? make_rsrc(static_cast<const uint16_t*>(a.w_scale) + u0 * 16,
+                                  (uint32_t)(((size_t)KB * N - u0 * 16) * 2))
+                      : sres;
   const __amdgpu_buffer_rsrc_t xres = make_rsrc(a.x, (uint32_t)((size_t)M * K * (FUSED ? 2 : 1)));
 
   // ---- fused quantize: load this thread's x chunks first, so that waiting
@@ -164,9 +198,12 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
     const uint32_t wv = ok ? (uint32_t)(lane * 16) : kOOB;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      wb[slot][t] = buf_load16s<kCacheStream>(wres, wv, (uint32_t)((t * KB + (ok ? kb : 0)) * kBlockBytes));
+      const bool up = SWIGLU && t >= HT;
+      const int tt = up ? t - HT : t;
+      wb[slot][t] = buf_load16s<kCacheStream>(up ? wres_u : wres, wv, (uint32_t)((tt * KB + (ok ? kb : 0)) * kBlockBytes));
       if constexpr (GROUP)
-        sgb[slot][t] = buf_load2s(sres, ok ? (uint32_t)((t * 16 + r16) * 2) : kOOB, (uint32_t)((size_t)(ok ? kb : 0) * N * 2));
+        sgb[slot][t] = buf_load2s(up ? sres_u : sres, ok ? (uint32_t)((tt * 16 + r16) * 2) : kOOB,
+                                  (uint32_t)((size_t)(ok ? kb : 0) * N * 2));
     }
     if constexpr (!FUSED) {
 #pragma unroll
@@ -192,19 +229,24 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
 
   // ---- epilogue scales, fetched now so their latency hides under the
   // weight stream.  Thread tid finishes outputs o = tid + q * threads.
-  constexpr int kOut = MT * 16 * NT * 16;
+  // Gated instances finish HT tiles of output columns, each from a gate
+  // and an up column.
+  constexpr int kOut = MT * 16 * HT * 16;
   constexpr int kOPT = (kOut + kThreads - 1) / kThreads;
   const bool scaled = a.out_kind != kOutI32;
-  const __amdgpu_buffer_rsrc_t swres =
-      make_rsrc(static_cast<const float*>(a.w_scale) + nt0 * 16, !GROUP && scaled ? (uint32_t)(tiles_here * 64) : 0u);
+  const __amdgpu_buffer_rsrc_t swres = make_rsrc(static_cast<const float*>(a.w_scale) + t0 * 16,
+                                                 !GROUP && scaled ? (uint32_t)((SWIGLU ? HT : tiles_here) * 64) : 0u);
+  const __amdgpu_buffer_rsrc_t swres_u =
+      make_rsrc(static_cast<const float*>(a.w_scale) + u0 * 16, !GROUP && SWIGLU ? (uint32_t)(HT * 64) : 0u);
   const __amdgpu_buffer_rsrc_t sxres = make_rsrc(a.x_scale, !FUSED && scaled ? (uint32_t)(M * 4) : 0u);
-  float swp[kOPT], sxp[kOPT];
+  float swp[kOPT], sxp[kOPT], swu[SWIGLU ? kOPT : 1];
 #pragma unroll
   for (int q = 0; q < kOPT; ++q) {
     const int o = tid + q * kThreads;
-    const int row = o / (NT * 16), col = o % (NT * 16);
+    const int row = o / (HT * 16), col = o % (HT * 16);
     const bool ok = o < kOut && row < M;
     swp[q] = __uint_as_float(buf_load4(swres, ok ? (uint32_t)(col * 4) : kOOB));
+    if constexpr (SWIGLU) swu[q] = __uint_as_float(buf_load4(swres_u, ok ? (uint32_t)(col * 4) : kOOB));
     sxp[q] = __uint_as_float(buf_load4(sxres, ok ? (uint32_t)(row * 4) : kOOB));
   }
 
@@ -366,32 +408,54 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   lds_barrier();
 
   const Emit emit{a};
+  auto wave_sum_f = [&](int mt, int t, int src) {
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) v += __uint_as_float(red[((w * MT + mt) * NT + t) * 256 + src]);
+    return v * 0.0625f;  // every partial and sum above is 16x the true one: exact barring underflow
+  };
+  auto wave_sum_i = [&](int mt, int t, int src) {
+    int v = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) v += (int)red[((w * MT + mt) * NT + t) * 256 + src];
+    return v;
+  };
 #pragma unroll
   for (int q = 0; q < kOPT; ++q) {
     const int o = tid + q * kThreads;
-    const int row = o / (NT * 16), col = o % (NT * 16);
+    const int row = o / (HT * 16), col = o % (HT * 16);
     const int mt = row >> 4, rr = row & 15, t = col >> 4, cc = col & 15;
     if (o >= kOut || row >= M || t >= tiles_here) continue;
     if constexpr (FUSED) sxp[q] = l_s[row];
     const int src = ((rr >> 2) * 16 + cc) * 4 + (rr & 3);
-    const int n = (nt0 + t) * 16 + cc;
+    const int n = (t0 + t) * 16 + cc;      // (gate) column
+    const int nu = (u0 + t) * 16 + cc;     // up column (gated instances)
     if constexpr (GROUP) {
-      float v = 0.0f;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) v += __uint_as_float(red[((w * MT + mt) * NT + t) * 256 + src]);
-      v *= 0.0625f;  // every partial and sum above is 16x the true one: exact barring underflow
-      if (a.S == 1)
-        emit.group(row, n, v, sxp[q]);
-      else
-        static_cast<float*>(a.partial)[((size_t)split * M + row) * N + n] = v;
+      const float v = wave_sum_f(mt, t, src);
+      const float vu = SWIGLU ? wave_sum_f(mt, t + HT, src) : 0.0f;
+      if (a.S == 1) {
+        if constexpr (SWIGLU)
+          emit.gated(row, n, __fmul_rn(v, sxp[q]), __fmul_rn(vu, sxp[q]));
+        else
+          emit.group(row, n, v, sxp[q]);
+      } else {
+        float* part = static_cast<float*>(a.partial) + ((size_t)split * M + row) * N;
+        part[n] = v;
+        if constexpr (SWIGLU) part[nu] = vu;
+      }
     } else {
-      int v = 0;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) v += (int)red[((w * MT + mt) * NT + t) * 256 + src];
-      if (a.S == 1)
-        emit.channel(row, n, v, sxp[q], swp[q]);
-      else
-        static_cast<int*>(a.partial)[((size_t)split * M + row) * N + n] = v;
+      const int v = wave_sum_i(mt, t, src);
+      const int vu = SWIGLU ? wave_sum_i(mt, t + HT, src) : 0;
+      if (a.S == 1) {
+        if constexpr (SWIGLU)
+          emit.gated(row, n, emit.channel_value(v, sxp[q], swp[q]), emit.channel_value(vu, sxp[q], swu[q]));
+        else
+          emit.channel(row, n, v, sxp[q], swp[q]);
+      } else {
+        int* part = static_cast<int*>(a.partial) + ((size_t)split * M + row) * N;
+        part[n] = v;
+        if constexpr (SWIGLU) part[nu] = vu;
+      }
     }
   }
   if (a.S == 1) return;
@@ -412,20 +476,33 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
 #pragma unroll
   for (int q = 0; q < kOPT; ++q) {
     const int o = tid + q * kThreads;
-    const int row = o / (NT * 16), col = o % (NT * 16);
+    const int row = o / (HT * 16), col = o % (HT * 16);
     const int t = col >> 4, cc = col & 15;
     if (o >= kOut || row >= M || t >= tiles_here) continue;
-    const int n = (nt0 + t) * 16 + cc;
+    const int n = (t0 + t) * 16 + cc;
+    const int nu = (u0 + t) * 16 + cc;
     if constexpr (GROUP) {
       const float* part = static_cast<const float*>(a.partial);
-      float v = 0.0f;
-      for (int s = 0; s < a.S; ++s) v += part[((size_t)s * M + row) * N + n];
-      emit.group(row, n, v, sxp[q]);
+      float v = 0.0f, vu = 0.0f;
+      for (int s = 0; s < a.S; ++s) {
+        v += part[((size_t)s * M + row) * N + n];
+        if constexpr (SWIGLU) vu += part[((size_t)s * M + row) * N + nu];
+      }
+      if constexpr (SWIGLU)
+        emit.gated(row, n, __fmul_rn(v, sxp[q]), __fmul_rn(vu, sxp[q]));
+      else
+        emit.group(row, n, v, sxp[q]);
     } else {
       const int* part = static_cast<const int*>(a.partial);
-      int v = 0;
-      for (int s = 0; s < a.S; ++s) v += part[((size_t)s * M + row) * N + n];
-      emit.channel(row, n, v, sxp[q], swp[q]);
+      int v = 0, vu = 0;
+      for (int s = 0; s < a.S; ++s) {
+        v += part[((size_t)s * M + row) * N + n];
+        if constexpr (SWIGLU) vu += part[((size_t)s * M + row) * N + nu];
+      }
+      if constexpr (SWIGLU)
+        emit.gated(row, n, emit.channel_value(v, sxp[q], swp[q]), emit.channel_value(vu, sxp[q], swu[q]));
+      else
+        emit.channel(row, n, v, sxp[q], swp[q]);
     }
   }
   if (tid == 0) __hip_atomic_store(&a.counters[gid], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -435,41 +512,45 @@ typedef void (*SmallMKernel)(const SmallMArgs);
 
 // MT * NT is capped at 12 (kMaxTilesPerWave): beyond it the accumulators
 // and in-flight operands no longer fit in 256 registers.  Group kernels
-// have no EXACT form (the planner never asks for one).
-template <int MT, int NT, bool GROUP, int QM>
+// have no EXACT form (the planner never asks for one); gated kernels need
+// an even NT.
+template <int MT, int NT, bool GROUP, int QM, bool SW>
 SmallMKernel instance(bool exact) {
-  if constexpr (MT * NT > kMaxTilesPerWave || (QM != kQNone && MT != 1))
+  if constexpr (MT * NT > kMaxTilesPerWave || (QM != kQNone && MT != 1) || (SW && NT % 2))
     return nullptr;
   else if constexpr (GROUP)
-    return exact ? nullptr : smallm<MT, NT, GROUP, QM, false>;
+    return exact ? nullptr : smallm<MT, NT, GROUP, QM, false, SW>;
   else
-    return exact ? smallm<MT, NT, GROUP, QM, true> : smallm<MT, NT, GROUP, QM, false>;
+    return exact ? smallm<MT, NT, GROUP, QM, true, SW> : smallm<MT, NT, GROUP, QM, false, SW>;
 }
 
-template <int MT, bool GROUP, int QM>
+template <int MT, bool GROUP, int QM, bool SW>
 SmallMKernel pick_nt(int NT, bool exact) {
   switch (NT) {
-    case 1: return instance<MT, 1, GROUP, QM>(exact);
-    case 2: return instance<MT, 2, GROUP, QM>(exact);
-    case 3: return instance<MT, 3, GROUP, QM>(exact);
-    case 4: return instance<MT, 4, GROUP, QM>(exact);
-    case 6: return instance<MT, 6, GROUP, QM>(exact);
+    case 1: return instance<MT, 1, GROUP, QM, SW>(exact);
+    case 2: return instance<MT, 2, GROUP, QM, SW>(exact);
+    case 3: return instance<MT, 3, GROUP, QM, SW>(exact);
+    case 4: return instance<MT, 4, GROUP, QM, SW>(exact);
+    case 6: return instance<MT, 6, GROUP, QM, SW>(exact);
     default: return nullptr;
   }
 }
 
-template <bool GROUP>
+template <bool GROUP, bool SW>
 SmallMKernel pick_group(const SmallMPlan& p) {
-  if (p.qmode == kQLds) return pick_nt<1, GROUP, kQLds>(p.NT, p.exact);
+  if (p.qmode == kQLds) return pick_nt<1, GROUP, kQLds, SW>(p.NT, p.exact);
   switch (p.MT) {
-    case 1: return pick_nt<1, GROUP, kQNone>(p.NT, p.exact);
-    case 2: return pick_nt<2, GROUP, kQNone>(p.NT, p.exact);
-    case 4: return pick_nt<4, GROUP, kQNone>(p.NT, p.exact);
+    case 1: return pick_nt<1, GROUP, kQNone, SW>(p.NT, p.exact);
+    case 2: return pick_nt<2, GROUP, kQNone, SW>(p.NT, p.exact);
+    case 4: return pick_nt<4, GROUP, kQNone, SW>(p.NT, p.exact);
     default: return nullptr;
   }
 }
 
-SmallMKernel pick(const SmallMPlan& p) { return p.group ? pick_group<true>(p) : pick_group<false>(p); }
+SmallMKernel pick(const SmallMPlan& p) {
+  if (p.swiglu) return p.group ? pick_group<true, true>(p) : pick_group<false, true>(p);
+  return p.group ? pick_group<true, false>(p) : pick_group<false, false>(p);
+}
 
 }  // namespace
 
@@ -489,17 +570,19 @@ constexpr double kHbmGBs = 6500.0;
 constexpr double kCuGBs = 60.0;
 constexpr double kSplitUs = 5.0;
 
-SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in) {
+SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in, bool swiglu) {
   SmallMPlan p{};
   p.MT = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   p.group = group;
+  p.swiglu = swiglu;
   const int ntiles = N / 16, KB = K / 128;
   const int nts[] = {1, 2, 3, 4, 6};
   const int ss[] = {1, 2, 4, 8};
   const double all_bytes = (double)N * K / 2;
   double best = 1e30;
   for (int nt : nts) {
-    if (ntiles % nt || p.MT * nt > kMaxTilesPerWave) continue;
+    // a gated group pairs nt / 2 gate tiles with the up tiles of the same columns
+    if (ntiles % nt || p.MT * nt > kMaxTilesPerWave || (swiglu && nt % 2)) continue;
     for (int s : ss) {
       if (s > KB) continue;
       const int kbs = (KB + s - 1) / s;
@@ -538,7 +621,7 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in) {
   // guarded loop, which measured faster for them even where no stage is
   // skipped (gate+up, M = 1 and 16).
   {
-    const int D = stage_depth(p.MT, p.NT, p.qmode, group);
+    const int D = stage_depth(p.MT, p.NT, p.qmode, group, swiglu);
     const int last = KB - (p.S - 1) * kbs;
     const int it_full = (kbs + kWaves - 1) / kWaves, it_last = (last + kWaves - 1) / kWaves;
     p.exact = !group && it_full % D == 0 && it_last % D == 0;
@@ -560,8 +643,8 @@ hipError_t launch_smallm(const SmallMPlan& p, const SmallMArgs& a, hipStream_t s
 const char* smallm_kernel_name(const SmallMPlan& p) {
   static thread_local char buf[96];
   static const char* modes[] = {"int8-in", "fused-quant"};
-  snprintf(buf, sizeof buf, "smallm<MT=%d,NT=%d,%s,%s> S=%d groups=%d", p.MT, p.NT,
-           p.group ? "group" : "channel", modes[p.qmode], p.S, p.groups);
+  snprintf(buf, sizeof buf, "smallm<MT=%d,NT=%d,%s,%s%s> S=%d groups=%d", p.MT, p.NT,
+           p.group ? "group" : "channel", modes[p.qmode], p.swiglu ? ",swiglu" : "", p.S, p.groups);
   return buf;
 }
 

@@ -31,6 +31,7 @@ struct SmallMArgs {
   int S, kbs;            // K splits and 128-k blocks per split
   int tpr;               // fused quantize: threads per token row
   int out_kind;
+  int F;                 // gated output: gate width (N / 2); y is [M][F]
 };
 struct SmallMPlan {
   int MT, NT;            // 16-row tiles, 16-column tiles per workgroup
@@ -41,9 +42,10 @@ struct SmallMPlan {
   int groups;            // workgroups along N
   int tpr;               // fused quantize: threads per token row
   bool exact;            // every wave's block count is a multiple of the stage depth
+  bool swiglu;           // gated output silu(gate) * up (gate columns [0, N/2), up [N/2, N))
   size_t lds_bytes;
 };
-SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in);
+SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in, bool swiglu);
 hipError_t launch_smallm(const SmallMPlan& p, const SmallMArgs& a, hipStream_t stream);
 constexpr int kSmallMWaves = 8;
 constexpr int kSmallMMaxM = 64;

@@ -126,3 +126,29 @@ def test_malformed_calls_are_rejected_without_launch():
     assert L.w4a8_quantize_act(None, 4, 256, fake, fake, None) == w.W4A8_EINVAL
     assert L.w4a8_pack_weights(fake, 250, 256, fake, None) == w.W4A8_EINVAL
     assert L.w4a8_pack_weights(None, 256, 256, fake, None) == w.W4A8_EINVAL
+
+
+def test_swiglu_plans_and_rejections():
+    # gate+up verify: the same column groups as the plain projection, gate
+    # and up tiles paired (NT even)
+    d = w.w4a8_linear_swiglu_describe(16, 24576, 4096)
+    assert "swiglu" in d and "NT=6" in d and "S=1" in d
+    assert w.w4a8_linear_swiglu_workspace_bytes(16, 24576, 4096) == w.w4a8_linear_workspace_bytes(16, 24576, 4096)
+    # odd tile counts per half are never paired across halves
+    for M, F, K in [(3, 48, 256), (1, 2048, 12288), (16, 16, 65536), (64, 80, 512)]:
+        d = w.w4a8_linear_swiglu_describe(M, 2 * F, K)
+        nt = int(d.split("NT=")[1].split(",")[0])
+        assert nt % 2 == 0 and (F // 16) % (nt // 2) == 0, d
+    # shapes the gated call rejects
+    assert w.w4a8_linear_swiglu_describe(65, 4096, 4096) == "invalid shape"
+    assert w.w4a8_linear_swiglu_describe(4, 48, 256) == "invalid shape"
+    assert w.w4a8_linear_swiglu_workspace_bytes(65, 4096, 4096) == 0
+    L = w.lib()
+    P = ctypes.c_void_p
+    fake = P(1 << 20)
+    f = L.w4a8_linear_swiglu
+    assert f(fake, 0, None, 65, 256, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EUNSUPPORTED
+    assert f(fake, 0, None, 4, 256, fake, fake, 0, 48, fake, 0, None, 0, None) == w.W4A8_EINVAL
+    assert f(fake, 0, None, 4, 256, fake, fake, 0, 256, fake, w.OUT_I32_ACC, None, 0, None) == w.W4A8_EINVAL
+    assert f(None, 0, None, 0, 256, None, None, 0, 256, None, 0, None, 0, None) == w.W4A8_OK
+    assert f(None, 0, None, 4, 256, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL

@@ -334,3 +334,57 @@ def test_threads_do_not_change_results():
     b = oracle.linear(x, W, s_g=sg, nthreads=5)
     for k in ("acc", "y32", "y", "y64"):
         np.testing.assert_array_equal(a[k], b[k])
+
+
+# ---------------------------------------------------------------- gated output
+
+def test_silu_mul_special_values():
+    g = np.array([0.0, -0.0, 1.0, -3.0, 50.0, -50.0, -800.0, 800.0])
+    u = np.array([5.0, 5.0, 0.0, 2.0, 3.0, 3.0, 7.0, 0.5])
+    y = oracle.silu_mul(g, u)
+    assert y[0] == 0.0 and y[1] == 0.0 and y[2] == 0.0
+    assert y[3] == pytest.approx(-3.0 / (1.0 + math.exp(3.0)) * 2.0, rel=1e-15)
+    assert y[4] == pytest.approx(150.0, rel=1e-15)              # silu(g) -> g for large g
+    assert abs(y[5]) < 1e-18 and y[5] < 0                       # silu(g) -> 0- for very negative g
+    assert y[6] == 0.0 and not np.isnan(y[6])                   # e^800 overflows: still exactly 0
+    assert y[7] == 400.0
+
+
+def test_silu_mul_matches_scipy_sigmoid():
+    # silu(g) = g * sigmoid(g); scipy's expit is an independent sigmoid
+    import scipy.special
+    r = rng(90)
+    g = np.concatenate([r.standard_normal(2000) * 4, np.linspace(-40, 40, 161)])
+    u = r.standard_normal(g.size)
+    np.testing.assert_allclose(oracle.silu_mul(g, u), g * scipy.special.expit(g) * u, rtol=2e-15, atol=1e-300)
+
+
+def test_silu_odd_part_is_identity():
+    # silu(g) - silu(-g) = g exactly in the reals: a dropped 1 in the
+    # denominator, or a missing factor g, breaks it (a sign slip in e^-g
+    # keeps it and is caught by the sigmoid and large-g pins above)
+    g = np.linspace(-30, 30, 601)
+    np.testing.assert_allclose(oracle.silu_mul(g, 1.0) - oracle.silu_mul(-g, 1.0), g, rtol=1e-14, atol=1e-14)
+
+
+def test_gated_output_halves_and_composition():
+    K, F = 384, 32
+    x = I.activations(5, K, 91)
+    r = rng(92)
+    Wg = r.integers(-7, 8, size=(F, K), dtype=np.int8)    # symmetric range: -Wg is valid too
+    Wu = r.integers(-8, 8, size=(F, K), dtype=np.int8)
+    sg = (r.random(F) * 0.02 + 0.001).astype(np.float32)
+    su = (r.random(F) * 0.02 + 0.001).astype(np.float32)
+    s = np.concatenate([sg, su])
+    pos = oracle.gated(oracle.linear(x, np.concatenate([Wg, Wu]), s_w=s))
+    neg = oracle.gated(oracle.linear(x, np.concatenate([-Wg, Wu]).astype(np.int8), s_w=s))
+    g = oracle.linear(x, Wg, s_w=sg)["y64"]
+    u = oracle.linear(x, Wu, s_w=su)["y64"]
+    # the halves are the separate projections (gate first, then up)
+    np.testing.assert_array_equal(pos["g64"], g)
+    np.testing.assert_array_equal(pos["u64"], u)
+    # odd part of silu: y(Wg) - y(-Wg) = g * u
+    np.testing.assert_allclose(pos["y64"] - neg["y64"], g * u, rtol=1e-12, atol=1e-12 * np.abs(g * u).max())
+    # a zero gate gives an exactly zero output whatever the up projection
+    zero = oracle.gated(oracle.linear(x, np.concatenate([np.zeros_like(Wg), Wu]), s_w=s))
+    assert not zero["y64"].any() and not zero["y_of32"].any()

@@ -80,11 +80,14 @@ class DirectCall:
     sizes), so a step costs one C call: the binding's per-call tensor checks
     would otherwise dominate a ~10 us kernel."""
 
-    def __init__(self, x, wps, w_scale, N, y, x_scale=None, workspace=None, out_kind=0, scale_mode=0):
+    def __init__(self, x, wps, w_scale, N, y, x_scale=None, workspace=None, out_kind=0, scale_mode=0,
+                 entry="w4a8_linear"):
         import ctypes
         import paper_2608_12932_amd as w
 
         self.L = w.lib()
+        self.fn = getattr(self.L, entry)
+        self.entry = entry
         self.M, self.K = x.shape
         self.in_kind = w.IN_I8 if x.dtype.is_floating_point is False else w.IN_BF16
         self.x = x.data_ptr()
@@ -95,7 +98,7 @@ class DirectCall:
         self.y = y.data_ptr()
         self.out_kind = out_kind
         self.scale_mode = scale_mode
-        need = w.w4a8_linear_workspace_bytes(self.M, N, self.K, scale_mode, self.in_kind)
+        need = int(getattr(self.L, entry + "_workspace_bytes")(self.M, N, self.K, scale_mode, self.in_kind))
         self.wk = None
         self.wk_bytes = 0
         buf = None
@@ -106,11 +109,31 @@ class DirectCall:
         self.c_size = ctypes.c_size_t
 
     def __call__(self, i, stream):
-        rc = self.L.w4a8_linear(self.x, self.in_kind, self.xs, self.M, self.K, self.wps[i % len(self.wps)],
-                                self.ws, self.scale_mode, self.N, self.y, self.out_kind,
-                                self.wk, self.wk_bytes, stream)
+        rc = self.fn(self.x, self.in_kind, self.xs, self.M, self.K, self.wps[i % len(self.wps)],
+                     self.ws, self.scale_mode, self.N, self.y, self.out_kind,
+                     self.wk, self.wk_bytes, stream)
         if rc:
-            raise RuntimeError(f"w4a8_linear failed: {rc}")
+            raise RuntimeError(f"{self.entry} failed: {rc}")
+
+
+def graph_ms(call, steps: int, reps: int = 20):
+    """ms per call of call(i, stream) captured reps times into one graph
+    (the calls cycle their weight copies as in eager timing) and replayed."""
+    import torch
+
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        call(0, cap.cuda_stream)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=cap):
+            for i in range(reps):
+                call(i, cap.cuda_stream)
+    torch.cuda.current_stream().wait_stream(cap)
+    ms = time_steps(lambda i: g.replay(), max(2, steps // reps), 2) / reps
+    del g
+    return ms
 
 
 def time_direct(call, steps: int, warmup: int):
@@ -262,6 +285,44 @@ def bench_down_verify(steps, warmup, copies=16):
     return {"workload": "down verify (down projection, draft-block verification)", "K": 12288, "N": 4096,
             "scales": "per-channel fp32", "x": "bf16 in, quantized in the step", "weight_copies": copies,
             "rows": rows}
+
+
+def bench_gate_up_swiglu(steps, warmup, copies=16):
+    """The gated gate+up projection (gate rows then up rows, N = 24576, K =
+    4096, per-channel scales) at M = 1 and 16: w4a8_linear_swiglu writes
+    silu(g) * u [M][12288] from the epilogue; the unfused form is
+    w4a8_linear to [M][24576] bf16 followed by torch's silu and multiply."""
+    import torch
+    import paper_2608_12932_amd as w
+
+    rows, cache = [], {}
+    for M in (1, 16):
+        xd, wps, sd, y, K, N, sbytes = _dev_inputs("gate_up_verify", M, 0, copies, cache)
+        F = N // 2
+        yg = torch.empty((M, F), dtype=torch.bfloat16, device=xd.device)
+        fused = DirectCall(xd, wps, sd, N, yg, workspace=w.Workspace(xd.device), entry="w4a8_linear_swiglu")
+        ms_fused = time_direct(fused, steps, warmup)
+        plain = DirectCall(xd, wps, sd, N, y, workspace=w.Workspace(xd.device))
+
+        def unfused(i, stream):
+            plain(i, stream)
+            torch.mul(torch.nn.functional.silu(y[:, :F]), y[:, F:], out=yg)
+
+        ms_unfused = time_direct(unfused, steps, warmup)
+        # the same two forms replayed from a graph (no host launch cost)
+        g_fused, g_unfused = graph_ms(fused, steps), graph_ms(unfused, steps)
+        nbytes = N * K // 2 + sbytes + M * K * 2 + M * F * 2
+        rows.append({"M": M, "us_fused": round(ms_fused * 1e3, 3), "us_unfused": round(ms_unfused * 1e3, 3),
+                     "us_fused_graph": round(g_fused * 1e3, 3), "us_unfused_graph": round(g_unfused * 1e3, 3),
+                     "GB/s_fused": round(nbytes / (ms_fused * 1e-3) / 1e9, 1),
+                     "frac_hbm_fused": round(nbytes / (ms_fused * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "algorithmic_bytes": nbytes, "kernel": w.w4a8_linear_swiglu_describe(M, N, K)})
+        del xd, wps, sd, y, yg, fused, plain
+    cache.clear()
+    torch.cuda.empty_cache()
+    return {"workload": "gated gate+up (silu(gate) * up merged into the projection's epilogue)", "K": 4096,
+            "N": 24576, "F": 12288, "scales": "per-channel fp32", "x": "bf16 in, quantized in the step",
+            "weight_copies": copies, "unfused": "w4a8_linear bf16 [M][N], then torch silu and mul", "rows": rows}
 
 
 def bench_layer_group(steps, warmup, copies=6):
@@ -444,6 +505,7 @@ def main():
     if args.sweep_only:
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
         print(json.dumps({"sweep": {"down_verify": bench_down_verify(ss, sw),
+                                    "gate_up_swiglu": bench_gate_up_swiglu(ss, sw),
                                     "layer_group": bench_layer_group(ss, sw),
                                     "stack": bench_stack(max(10, args.steps // 50))}}), flush=True)
         return
@@ -496,7 +558,8 @@ def main():
     out["ceilings"] = measure_ceilings()
     if not args.no_sweep:
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
-        out["sweep"] = {"down_verify": bench_down_verify(ss, sw), "layer_group": bench_layer_group(ss, sw),
+        out["sweep"] = {"down_verify": bench_down_verify(ss, sw), "gate_up_swiglu": bench_gate_up_swiglu(ss, sw),
+                        "layer_group": bench_layer_group(ss, sw),
                         "stack": bench_stack(max(10, args.steps // 50))}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(d, algo_bytes)

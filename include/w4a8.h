@@ -179,9 +179,9 @@ const char* w4a8_linear_describe(int64_t M, int64_t N, int64_t K, int scale_mode
  *   - y is [M][N/2] of out_kind, W4A8_OUT_BF16 or W4A8_OUT_F32.
  *   - N % 32 == 0 (whole 16-column tiles in each half); other arguments and
  *     the workspace as for w4a8_linear, with its own size query below.
- *   - The decode / draft-block verification path only: 1 <= M <= 64
- *     (W4A8_EUNSUPPORTED above; M == 0 is a no-op).  W4A8_OUT_I32_ACC and
- *     N % 32 != 0 are W4A8_EINVAL.
+ *     W4A8_OUT_I32_ACC and N % 32 != 0 are W4A8_EINVAL; M == 0 is a no-op.
+ *   - Every M the plain call takes: M <= 64 runs the small-M kernels,
+ *     larger M the large-M kernel on its 128 x 128 tile.
  * Does not synchronize; enqueues kernels only (graph-capturable), like
  * w4a8_linear.
  */

@@ -33,7 +33,6 @@ struct Plan {
   size_t off_counters = 0, off_partial = 0, off_xq = 0, off_sx = 0, total = 0;
 };
 
-// Gated plans (swiglu) exist only for M <= kSmallMMaxM.
 Plan make_plan(int64_t M, int64_t N, int64_t K, bool group, bool bf16_in, bool swiglu = false) {
   Plan p;
   p.small_m = M <= kSmallMMaxM;
@@ -48,7 +47,7 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, bool group, bool bf16_in, bool s
       off = round_up(off + (size_t)p.sm.S * M * N * 4, 256);
     }
   } else {
-    p.lm = plan_largem((int)M, (int)N, (int)K, group);
+    p.lm = plan_largem((int)M, (int)N, (int)K, group, swiglu);
     p.separate_quant = bf16_in;
   }
   if (p.separate_quant) {
@@ -69,8 +68,8 @@ bool valid_modes(int scale_mode, int in_kind) {
 }
 
 // Shapes the gated entry points take: an even number of 16-column tiles
-// (gate and up halves of whole tiles) and the small-M path.
-bool gated_shape(int64_t M, int64_t N) { return N % 32 == 0 && M <= kSmallMMaxM; }
+// (gate and up halves of whole tiles).
+bool gated_shape(int64_t N) { return N % 32 == 0; }
 
 // Both linear entry points after their own checks: the rest of the
 // validation, the plan, and the launches.
@@ -84,7 +83,6 @@ w4a8_status run_linear(const void* x, int in_kind, const float* x_scale, int64_t
     return W4A8_EINVAL;
   if (swiglu && (out_kind == W4A8_OUT_I32_ACC || N % 32)) return W4A8_EINVAL;
   if (M == 0) return W4A8_OK;
-  if (swiglu && M > kSmallMMaxM) return W4A8_EUNSUPPORTED;
   // 32-bit buffer offsets: the group-scale array (N*K/64 bytes) stays below 2 GiB
   if ((uint64_t)N * (uint64_t)K >= (uint64_t(1) << 37)) return W4A8_EUNSUPPORTED;
   if (!x || !aligned(x, 16) || !w_packed || !aligned(w_packed, 16) || !y || !aligned(y, 16))
@@ -149,6 +147,7 @@ w4a8_status run_linear(const void* x, int in_kind, const float* x_scale, int64_t
     a.tiles_m = p.lm.tiles_m;
     a.tiles_n = p.lm.tiles_n;
     a.xcd_remap = (p.lm.tiles_m * p.lm.tiles_n) % 8 == 0;
+    a.F = swiglu ? (int)(N / 2) : 0;
     e = launch_largem(p.lm, a, stream);
   }
   return e == hipSuccess ? W4A8_OK : W4A8_EHIP;
@@ -157,14 +156,14 @@ w4a8_status run_linear(const void* x, int in_kind, const float* x_scale, int64_t
 size_t workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind, bool swiglu) {
   if (M < 0 || M > W4A8_M_MAX || !valid_nk(N, K) || !valid_modes(scale_mode, in_kind)) return 0;
   if (M == 0 || (uint64_t)N * (uint64_t)K >= (uint64_t(1) << 37)) return 0;
-  if (swiglu && !gated_shape(M, N)) return 0;
+  if (swiglu && !gated_shape(N)) return 0;
   return make_plan(M, N, K, scale_mode == W4A8_SCALE_GROUP_F16, in_kind == W4A8_IN_BF16, swiglu).total;
 }
 
 const char* describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind, int out_kind, bool swiglu) {
   static thread_local char buf[256];
   if (M <= 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return "invalid shape";
-  if (swiglu && !gated_shape(M, N)) return "invalid shape";
+  if (swiglu && !gated_shape(N)) return "invalid shape";
   const bool group = scale_mode == W4A8_SCALE_GROUP_F16 && out_kind != W4A8_OUT_I32_ACC;
   const Plan p = make_plan(M, N, K, group, in_kind == W4A8_IN_BF16, swiglu);
   snprintf(buf, sizeof buf, "%s%s workspace=%zu", p.separate_quant ? "quantize_rows + " : "",

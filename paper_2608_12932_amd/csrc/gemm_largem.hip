@@ -9,7 +9,8 @@ namespace w4a8 {
 
 namespace {
 
-LargeMKernelFn channel_kernel(int cfg) {
+LargeMKernelFn channel_kernel(int cfg, bool swiglu) {
+  if (swiglu) return cfg == kGatedCfg ? menu_kernel<kGatedCfg, false, true>() : nullptr;
   switch (cfg) {
     case 0: return menu_kernel<0, false>();
     case 1: return menu_kernel<1, false>();
@@ -20,16 +21,20 @@ LargeMKernelFn channel_kernel(int cfg) {
 
 }  // namespace
 
-LargeMPlan plan_largem(int M, int N, int K, bool group) {
+// Gated plans (swiglu) take the 128 x 128 tile, whose waves hold a gate and
+// an up block each: a tile covers 64 output columns.
+LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu) {
   (void)K;
   LargeMPlan p{};
   p.group = group;
+  p.swiglu = swiglu;
   double best = -1.0;
   for (int c = 0; c < kMenuSize; ++c) {
     const TileCfg& t = kMenu[c];
     if (group && !t.group_ok) continue;
+    if (swiglu && c != kGatedCfg) continue;
     const int BM = 32 * t.WM * t.GM, BN = 32 * t.WN * t.GN;
-    const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
+    const int tm = (M + BM - 1) / BM, tn = swiglu ? (N / 2 + BN / 2 - 1) / (BN / 2) : (N + BN - 1) / BN;
     const long tiles = (long)tm * tn;
     const long rounds = (tiles + 255) / 256;
     const double eff = (double)M * N / ((double)rounds * 256.0 * BM * BN);
@@ -50,7 +55,7 @@ LargeMPlan plan_largem(int M, int N, int K, bool group) {
 }
 
 hipError_t launch_largem(const LargeMPlan& p, const LargeMArgs& a, hipStream_t stream) {
-  LargeMKernelFn k = p.group ? largem_group_kernel(p.cfg) : channel_kernel(p.cfg);
+  LargeMKernelFn k = p.group ? largem_group_kernel(p.cfg, p.swiglu) : channel_kernel(p.cfg, p.swiglu);
   if (!k) return hipErrorInvalidValue;
   const unsigned grid = (unsigned)(p.tiles_m * p.tiles_n);
   hipLaunchKernelGGL(k, dim3(grid), dim3(p.threads), p.lds_bytes, stream, a);
@@ -59,8 +64,8 @@ hipError_t launch_largem(const LargeMPlan& p, const LargeMArgs& a, hipStream_t s
 
 const char* largem_kernel_name(const LargeMPlan& p) {
   static thread_local char buf[96];
-  snprintf(buf, sizeof buf, "largem<%dx%d,%s> tiles=%dx%d", p.BM, p.BN, p.group ? "group" : "channel",
-           p.tiles_m, p.tiles_n);
+  snprintf(buf, sizeof buf, "largem<%dx%d,%s%s> tiles=%dx%d", p.BM, p.BN, p.group ? "group" : "channel",
+           p.swiglu ? ",swiglu" : "", p.tiles_m, p.tiles_n);
   return buf;
 }
 

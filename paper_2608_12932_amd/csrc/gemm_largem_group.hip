@@ -10,7 +10,8 @@
 
 namespace w4a8 {
 
-LargeMKernelFn largem_group_kernel(int cfg) {
+LargeMKernelFn largem_group_kernel(int cfg, bool swiglu) {
+  if (swiglu) return cfg == kGatedCfg ? menu_kernel<kGatedCfg, true, true>() : nullptr;
   switch (cfg) {
     case 1: return menu_kernel<1, true>();
     case 2: return menu_kernel<2, true>();

@@ -61,20 +61,23 @@ struct LargeMArgs {
   int out_kind;
   int tiles_m, tiles_n;
   int xcd_remap;
+  int F;                 // gated output: gate width (N / 2); y is [M][F]
 };
 struct LargeMPlan {
   int cfg;               // index into the tile menu
   int BM, BN, threads;
   bool group;
+  bool swiglu;           // gated output (the 128 x 128 tile; a tile covers BN / 2 output columns)
   int tiles_m, tiles_n;
   size_t lds_bytes;
 };
-LargeMPlan plan_largem(int M, int N, int K, bool group);
+LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu);
 hipError_t launch_largem(const LargeMPlan& p, const LargeMArgs& a, hipStream_t stream);
 typedef void (*LargeMKernelFn)(const LargeMArgs);
 // group-scale instance of tile-menu entry cfg (gemm_largem_group.hip), or
-// nullptr where the tile does not fit the group accumulators
-LargeMKernelFn largem_group_kernel(int cfg);
+// nullptr where the tile does not fit the group accumulators (or, gated,
+// for any tile but the gated one)
+LargeMKernelFn largem_group_kernel(int cfg, bool swiglu);
 
 const char* smallm_kernel_name(const SmallMPlan& p);
 const char* largem_kernel_name(const LargeMPlan& p);

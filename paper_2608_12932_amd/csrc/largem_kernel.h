@@ -33,6 +33,11 @@
 // each step's int32 partial is rescaled by its fp16 group scale into an
 // fp32 accumulator), stages the output tile in the idle LDS ring and writes
 // it as 16-byte row chunks.
+// SW (gated) instances serve the fused gate+up projection with its gated
+// activation merged in (FlashDrive Sec. 3.5, Kernel Fusion): with two
+// 32-column blocks per wave (WN = 2), block 0 holds gate columns and block
+// 1 the up columns of the same outputs, and the tile writes silu(g) * u,
+// BN / 2 columns of y.
 #pragma once
 #include <type_traits>
 
@@ -61,8 +66,9 @@ constexpr TileCfg kMenu[] = {
 };
 constexpr int kMenuSize = sizeof(kMenu) / sizeof(kMenu[0]);
 
-template <int WM, int WN, int GM, int GN, bool GROUP, int kRing>
+template <int WM, int WN, int GM, int GN, bool GROUP, int kRing, bool SW>
 __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
+  static_assert(!SW || WN == 2, "gated tiles pair one gate and one up block per wave");
   constexpr int kThreads = GM * GN * 64;
   constexpr int kWaves = GM * GN;
   constexpr int BM = 32 * WM * GM, BN = 32 * WN * GN;
@@ -82,7 +88,11 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   const int total = a.tiles_m * a.tiles_n;
   if (a.xcd_remap) bid = (bid & 7) * (total >> 3) + (bid >> 3);
   const int tm = bid % a.tiles_m, tn = bid / a.tiles_m;
+  // Gated tiles: tile columns [0, BN/2) are gate columns f0 .., [BN/2, BN)
+  // the up columns F + f0 ..; output columns f0 .. f0 + BN/2.
+  constexpr int OBN = SW ? BN / 2 : BN;  // output columns per tile
   const int m0 = tm * BM, n0 = tn * BN, nt0 = n0 / 16;
+  const int f0 = tn * OBN, ft0 = f0 / 16, fu0 = a.F / 16 + ft0;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % GM, wn = wave / GM;
@@ -93,12 +103,20 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   // Per-tile buffer descriptors: rows past M and tiles past N lie outside
   // them and read as zeros (no branch, no traffic).
   const int rows_here = min(BM, M - m0);
-  const int tiles_here = min(BN / 16, ntiles - nt0);
-  const int cols_here = min(BN, N - n0);
+  // (gated: per half, the tiles and columns inside [0, F))
+  const int tiles_here = SW ? min(OBN / 16, a.F / 16 - ft0) : min(BN / 16, ntiles - nt0);
+  const int cols_here = SW ? min(OBN, a.F - f0) : min(BN, N - n0);
   const u32x4 ares = make_rsrc_words(a.xq + (size_t)m0 * K, (uint32_t)(rows_here * K));
-  const u32x4 bres = make_rsrc_words(a.wp + (size_t)nt0 * KB * kBlockBytes, (uint32_t)(tiles_here * KB * kBlockBytes));
-  const u32x4 sres = make_rsrc_words(static_cast<const uint16_t*>(a.w_scale) + n0,
-                                     GROUP ? (uint32_t)(((size_t)KB * N - n0) * 2) : 0u);
+  const u32x4 bres = make_rsrc_words(a.wp + (size_t)(SW ? ft0 : nt0) * KB * kBlockBytes,
+                                     (uint32_t)(tiles_here * KB * kBlockBytes));
+  const u32x4 bres_u =
+      SW ? make_rsrc_words(a.wp + (size_t)fu0 * KB * kBlockBytes, (uint32_t)(tiles_here * KB * kBlockBytes)) : bres;
+  const int sc0 = SW ? f0 : n0, scu = SW ? a.F + f0 : n0;  // first scale column of each half
+  const u32x4 sres = make_rsrc_words(static_cast<const uint16_t*>(a.w_scale) + sc0,
+                                     GROUP ? (uint32_t)(((size_t)KB * N - sc0) * 2) : 0u);
+  const u32x4 sres_u = SW ? make_rsrc_words(static_cast<const uint16_t*>(a.w_scale) + scu,
+                                            GROUP ? (uint32_t)(((size_t)KB * N - scu) * 2) : 0u)
+                          : sres;
   const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
 
   // Load j of this thread for the A part covers LDS chunk p = j * threads +
@@ -112,16 +130,25 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
     a_voff[j] = (uint32_t)(row * K + ch * 16);
   }
   // group scales: wave w fetches columns [w kSPerWave, +kSPerWave), two per
-  // lane (4 bytes); lanes past that and columns past N read zeros
-  const int scol = wave * kSPerWave + 2 * lane;
+  // lane (4 bytes); lanes past that and columns past N read zeros.  Gated
+  // tiles: the waves of the second half fetch the up columns.
+  const bool s_up = SW && wave * kSPerWave >= OBN;
+  const int scol = wave * kSPerWave - (s_up ? OBN : 0) + 2 * lane;
   const uint32_t s_voff = GROUP && 2 * lane < kSPerWave && scol < cols_here ? (uint32_t)(scol * 2) : kOOB;
 
   // Vector-memory instruction d of step kb's stage fill (A loads, then B
   // loads, then the group scales).  Past the end the loads read zeros
   // without traffic, so every step issues the same kPerStage instructions.
+  // Gated tiles: blocks [0, BN/32) of the stage are gate tiles, the rest the
+  // up tiles of the same columns.
   uint32_t b_voff[kBCh];
+  bool b_up[kBCh];
 #pragma unroll
-  for (int j = 0; j < kBCh; ++j) b_voff[j] = (uint32_t)(lane * 16 + (j * kWaves + wave) * KB * kBlockBytes);
+  for (int j = 0; j < kBCh; ++j) {
+    const int blk = j * kWaves + wave;
+    b_up[j] = SW && blk >= BN / 32;
+    b_voff[j] = (uint32_t)(lane * 16 + (blk - (b_up[j] ? BN / 32 : 0)) * KB * kBlockBytes);
+  }
   // A step past the end gets the scalar offset kOOB: every lane's offset
   // then lies past the descriptor's range (no vector select needed).
   auto issue_one = [&](int kb, int d) {
@@ -131,22 +158,26 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
       lds_dma16(ares, st + (d * kWaves + wave) * 1024, a_voff[d], ok ? kb * 128 : kOOB);
     } else if (d < kACh + kBCh) {
       const int blk = (d - kACh) * kWaves + wave;
-      lds_dma16_nt(bres, st + kABytes + blk * 1024, b_voff[d - kACh], ok ? kb * kBlockBytes : kOOB);
+      lds_dma16_nt(b_up[d - kACh] ? bres_u : bres, st + kABytes + blk * 1024, b_voff[d - kACh],
+                   ok ? kb * kBlockBytes : kOOB);
     } else if constexpr (GROUP) {
-      lds_dma4(sres, st + kABytes + kBBytes + wave * 256, s_voff, ok ? (uint32_t)((size_t)kb * N * 2) : kOOB);
+      lds_dma4(s_up ? sres_u : sres, st + kABytes + kBBytes + wave * 256, s_voff,
+               ok ? (uint32_t)((size_t)kb * N * 2) : kOOB);
     }
   };
 
   // LDS read offsets of this lane's MFMA operands: activation row
   // wm 32 WM + 32 i + l32 (its chunks c sit at c ^ ((row >> 1) & 7)), weight column
-  // wn 32 WN + 32 j + l32 of the stage's weight tiles.
+  // wn 32 WN + 32 j + l32 of the stage's weight tiles (gated: column
+  // j BN/2 + 32 wn + l32, block 0 in the gate half, block 1 in the up half).
+  auto tile_col = [&](int j) { return SW ? j * (BN / 2) + wn * 32 + l32 : wn * 32 * WN + j * 32 + l32; };
   const int swz = (l32 >> 1) & 7;
   uint32_t a_rd[WM], b_rd[WN];
 #pragma unroll
   for (int i = 0; i < WM; ++i) a_rd[i] = (uint32_t)((wm * 32 * WM + i * 32 + l32) * 128);
 #pragma unroll
   for (int j = 0; j < WN; ++j) {
-    const int col = wn * 32 * WN + j * 32 + l32;
+    const int col = tile_col(j);
     b_rd[j] = (uint32_t)(kABytes + (col >> 4) * kBlockBytes + (col & 15) * 16);
   }
   // MFMA k half tp covers the 64 k of chunk group g = 2 tp + g2: activation
@@ -161,7 +192,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   uint32_t s_rd[GROUP ? WN : 1];
 #pragma unroll
   for (int j = 0; j < (GROUP ? WN : 1); ++j) {
-    const int col = wn * 32 * WN + j * 32 + l32;
+    const int col = tile_col(j);
     s_rd[j] = (uint32_t)(kABytes + kBBytes + (col / kSPerWave) * 256 + (col % kSPerWave) * 2);
   }
 
@@ -211,12 +242,15 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   const bool scaled = a.out_kind != kOutI32;
   const __amdgpu_buffer_rsrc_t xsres =
       make_rsrc(uniform_ptr(a.x_scale + m0), uniform_u32(scaled ? (uint32_t)(rows_here * 4) : 0u));
-  const __amdgpu_buffer_rsrc_t wsres = make_rsrc(uniform_ptr(static_cast<const float*>(a.w_scale) + n0),
+  const __amdgpu_buffer_rsrc_t wsres = make_rsrc(uniform_ptr(static_cast<const float*>(a.w_scale) + sc0),
                                                  uniform_u32((!GROUP && scaled) ? (uint32_t)(cols_here * 4) : 0u));
+  const __amdgpu_buffer_rsrc_t wsres_u = make_rsrc(uniform_ptr(static_cast<const float*>(a.w_scale) + scu),
+                                                   uniform_u32((SW && !GROUP) ? (uint32_t)(cols_here * 4) : 0u));
   float swv[WN];
 #pragma unroll
   for (int j = 0; j < WN; ++j)
-    swv[j] = __uint_as_float(buf_load4(wsres, (uint32_t)((wn * 32 * WN + j * 32 + l32) * 4)));
+    swv[j] = SW ? __uint_as_float(buf_load4(j ? wsres_u : wsres, (uint32_t)((wn * 32 + l32) * 4)))
+                : __uint_as_float(buf_load4(wsres, (uint32_t)((wn * 32 * WN + j * 32 + l32) * 4)));
   uint4 sx4[WM][4];
   auto load_sx = [&]() {
 #pragma unroll
@@ -449,11 +483,23 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
       return __fmul_rn(__fmul_rn((float)(acc[0][i][j][r] >> 4), sx), swv[j]);
     }
   };
+  // The output tile: OWN 32-column blocks per wave (gated: one, the
+  // activation of the gate block and the up block).
+  constexpr int OWN = SW ? 1 : WN;
+  auto out_value = [&](int i, int j, int r) -> float {
+    if constexpr (SW) {
+      const float g = result(i, 0, r), u = result(i, 1, r);
+      return __fmul_rn(__fdiv_rn(g, __fadd_rn(1.0f, __expf(-g))), u);
+    } else {
+      return result(i, j, r);
+    }
+  };
+  const int ldy = SW ? a.F : N, oc0 = SW ? f0 : n0;  // output row stride, first output column
   auto store_tile = [&](auto es_tag) {
     constexpr int es = decltype(es_tag)::value;  // output element bytes
     // Row pitch: one half-wave's writes (bf16: rows R and R + 1 of 64 bytes;
     // 4-byte kinds: one 128-byte row) cover all 32 banks once.
-    constexpr int kPitch = es == 2 ? BN * 2 + 64 : BN * 4 + 16;
+    constexpr int kPitch = es == 2 ? OBN * 2 + 64 : OBN * 4 + 16;
     static_assert(BM * kPitch <= kRing * kStage, "output tile must fit the LDS ring");
     if constexpr (es == 2) {
       // NaN results become the canonical quiet NaN (sign and payload of a NaN
@@ -468,36 +514,37 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
-        for (int j = 0; j < WN; ++j)
+        for (int j = 0; j < OWN; ++j)
 #pragma unroll
           for (int rp = 0; rp < 8; ++rp) {
-            const uint32_t pair = bf16x2_bits(canonical_nan(result(i, j, 2 * rp)), canonical_nan(result(i, j, 2 * rp + 1)));
+            const uint32_t pair =
+                bf16x2_bits(canonical_nan(out_value(i, j, 2 * rp)), canonical_nan(out_value(i, j, 2 * rp + 1)));
             const uint32_t recv = (uint32_t)__builtin_amdgcn_mov_dpp((int)pair, 0xB1, 0xF, 0xF, false);
             const uint32_t word = __builtin_amdgcn_perm(recv, pair, sel);
             const int r = 2 * rp + (odd ? 1 : 0);
             const int row = wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3);
-            const int col = wn * 32 * WN + j * 32 + (l32 & ~1);
+            const int col = wn * 32 * OWN + j * 32 + (l32 & ~1);
             *reinterpret_cast<uint32_t*>(lds + row * kPitch + col * 2) = word;
           }
     } else {
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
-        for (int j = 0; j < WN; ++j)
+        for (int j = 0; j < OWN; ++j)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int row = wm * 32 * WM + i * 32 + 8 * (r >> 2) + 4 * g2 + (r & 3);
-            const int col = wn * 32 * WN + j * 32 + l32;
+            const int col = wn * 32 * OWN + j * 32 + l32;
             uint32_t v;
-            if constexpr (GROUP)
-              v = __float_as_uint(result(i, j, r));
+            if constexpr (GROUP || SW)
+              v = __float_as_uint(out_value(i, j, r));
             else
               v = a.out_kind == kOutI32 ? (uint32_t)(acc[0][i][j][r] >> 4) : __float_as_uint(result(i, j, r));
             *reinterpret_cast<uint32_t*>(lds + row * kPitch + col * 4) = v;
           }
     }
     lds_barrier();
-    constexpr int kRowChunks = BN * es / 16;
+    constexpr int kRowChunks = OBN * es / 16;
     constexpr int kChunks = BM * kRowChunks;
     static_assert(kChunks % kThreads == 0, "output chunks must split evenly over the threads");
 #pragma unroll
@@ -508,7 +555,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
       // N is a multiple of 16 and a chunk holds 4 or 8 columns, so a chunk
       // is either wholly inside the output or wholly past its last column
       if (row < rows_here && cc * (16 / es) < cols_here)
-        *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.y) + ((size_t)(m0 + row) * N + n0) * es + cc * 16) = v;
+        *reinterpret_cast<uint4*>(static_cast<uint8_t*>(a.y) + ((size_t)(m0 + row) * ldy + oc0) * es + cc * 16) = v;
     }
   };
   if (a.out_kind == kOutBF16)
@@ -517,11 +564,13 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
     store_tile(std::integral_constant<int, 4>{});
 }
 
-// The instance of menu entry C.
-template <int C, bool GROUP>
+// The instance of menu entry C (SW: the gated form).
+template <int C, bool GROUP, bool SW = false>
 constexpr LargeMKernelFn menu_kernel() {
-  return largem<kMenu[C].WM, kMenu[C].WN, kMenu[C].GM, kMenu[C].GN, GROUP, kMenu[C].ring>;
+  return largem<kMenu[C].WM, kMenu[C].WN, kMenu[C].GM, kMenu[C].GN, GROUP, kMenu[C].ring, SW>;
 }
+// The tile the gated instances use: 128 x 128, two blocks per wave.
+constexpr int kGatedCfg = 1;
 
 }  // namespace
 

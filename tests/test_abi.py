@@ -139,15 +139,19 @@ def test_swiglu_plans_and_rejections():
         d = w.w4a8_linear_swiglu_describe(M, 2 * F, K)
         nt = int(d.split("NT=")[1].split(",")[0])
         assert nt % 2 == 0 and (F // 16) % (nt // 2) == 0, d
+    # large M: the 128 x 128 tile, 64 output columns per tile
+    d = w.w4a8_linear_swiglu_describe(1024, 24576, 4096)
+    assert "largem<128x128,channel,swiglu>" in d and "tiles=8x192" in d, d
+    assert "largem<128x128,group,swiglu> tiles=1x2" in w.w4a8_linear_swiglu_describe(65, 160, 256, 1)
+    assert w.w4a8_linear_swiglu_workspace_bytes(1024, 24576, 4096) == w.w4a8_linear_workspace_bytes(1024, 24576, 4096)
     # shapes the gated call rejects
-    assert w.w4a8_linear_swiglu_describe(65, 4096, 4096) == "invalid shape"
     assert w.w4a8_linear_swiglu_describe(4, 48, 256) == "invalid shape"
-    assert w.w4a8_linear_swiglu_workspace_bytes(65, 4096, 4096) == 0
+    assert w.w4a8_linear_swiglu_workspace_bytes(4, 48, 256) == 0
     L = w.lib()
     P = ctypes.c_void_p
     fake = P(1 << 20)
     f = L.w4a8_linear_swiglu
-    assert f(fake, 0, None, 65, 256, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EUNSUPPORTED
+    assert f(fake, 0, None, 1024, 4096, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL  # no workspace
     assert f(fake, 0, None, 4, 256, fake, fake, 0, 48, fake, 0, None, 0, None) == w.W4A8_EINVAL
     assert f(fake, 0, None, 4, 256, fake, fake, 0, 256, fake, w.OUT_I32_ACC, None, 0, None) == w.W4A8_EINVAL
     assert f(None, 0, None, 0, 256, None, None, 0, 256, None, 0, None, 0, None) == w.W4A8_OK

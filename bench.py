@@ -289,14 +289,15 @@ def bench_down_verify(steps, warmup, copies=16):
 
 def bench_gate_up_swiglu(steps, warmup, copies=16):
     """The gated gate+up projection (gate rows then up rows, N = 24576, K =
-    4096, per-channel scales) at M = 1 and 16: w4a8_linear_swiglu writes
-    silu(g) * u [M][12288] from the epilogue; the unfused form is
-    w4a8_linear to [M][24576] bf16 followed by torch's silu and multiply."""
+    4096, per-channel scales) at M = 1 and 16 (verify / decode) and 1024
+    (prefill): w4a8_linear_swiglu writes silu(g) * u [M][12288] from the
+    epilogue; the unfused form is w4a8_linear to [M][24576] bf16 followed by
+    torch's silu and multiply."""
     import torch
     import paper_2608_12932_amd as w
 
     rows, cache = [], {}
-    for M in (1, 16):
+    for M in (1, 16, 1024):
         xd, wps, sd, y, K, N, sbytes = _dev_inputs("gate_up_verify", M, 0, copies, cache)
         F = N // 2
         yg = torch.empty((M, F), dtype=torch.bfloat16, device=xd.device)
@@ -314,6 +315,7 @@ def bench_gate_up_swiglu(steps, warmup, copies=16):
         nbytes = N * K // 2 + sbytes + M * K * 2 + M * F * 2
         rows.append({"M": M, "us_fused": round(ms_fused * 1e3, 3), "us_unfused": round(ms_unfused * 1e3, 3),
                      "us_fused_graph": round(g_fused * 1e3, 3), "us_unfused_graph": round(g_unfused * 1e3, 3),
+                     "TOPS_fused": round(2 * M * N * K / (ms_fused * 1e-3) / 1e12, 1),
                      "GB/s_fused": round(nbytes / (ms_fused * 1e-3) / 1e9, 1),
                      "frac_hbm_fused": round(nbytes / (ms_fused * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "algorithmic_bytes": nbytes, "kernel": w.w4a8_linear_swiglu_describe(M, N, K)})

@@ -10,7 +10,13 @@ namespace w4a8 {
 namespace {
 
 LargeMKernelFn channel_kernel(int cfg, bool swiglu) {
-  if (swiglu) return cfg == kGatedCfg ? menu_kernel<kGatedCfg, false, true>() : nullptr;
+  if (swiglu) {
+    switch (cfg) {
+      case 1: return menu_kernel<1, false, true>();
+      case 3: return menu_kernel<3, false, true>();
+      default: return nullptr;
+    }
+  }
   switch (cfg) {
     case 0: return menu_kernel<0, false>();
     case 1: return menu_kernel<1, false>();
@@ -21,8 +27,8 @@ LargeMKernelFn channel_kernel(int cfg, bool swiglu) {
 
 }  // namespace
 
-// Gated plans (swiglu) take the 128 x 128 tile, whose waves hold a gate and
-// an up block each: a tile covers 64 output columns.
+// Gated plans (swiglu) take the tiles whose waves hold an even number of
+// blocks (gate and up halves): a tile covers BN / 2 output columns.
 LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu) {
   (void)K;
   LargeMPlan p{};
@@ -32,7 +38,7 @@ LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu) {
   for (int c = 0; c < kMenuSize; ++c) {
     const TileCfg& t = kMenu[c];
     if (group && !t.group_ok) continue;
-    if (swiglu && c != kGatedCfg) continue;
+    if (swiglu ? !t.gated_ok : !t.plain_ok) continue;
     const int BM = 32 * t.WM * t.GM, BN = 32 * t.WN * t.GN;
     const int tm = (M + BM - 1) / BM, tn = swiglu ? (N / 2 + BN / 2 - 1) / (BN / 2) : (N + BN - 1) / BN;
     const long tiles = (long)tm * tn;

@@ -11,7 +11,7 @@
 namespace w4a8 {
 
 LargeMKernelFn largem_group_kernel(int cfg, bool swiglu) {
-  if (swiglu) return cfg == kGatedCfg ? menu_kernel<kGatedCfg, true, true>() : nullptr;
+  if (swiglu) return cfg == 1 ? menu_kernel<1, true, true>() : nullptr;  // the gated tile that fits group mode
   switch (cfg) {
     case 1: return menu_kernel<1, true>();
     case 2: return menu_kernel<2, true>();

@@ -34,9 +34,9 @@
 // fp32 accumulator), stages the output tile in the idle LDS ring and writes
 // it as 16-byte row chunks.
 // SW (gated) instances serve the fused gate+up projection with its gated
-// activation merged in (FlashDrive Sec. 3.5, Kernel Fusion): with two
-// 32-column blocks per wave (WN = 2), block 0 holds gate columns and block
-// 1 the up columns of the same outputs, and the tile writes silu(g) * u,
+// activation merged in (FlashDrive Sec. 3.5, Kernel Fusion): of a wave's WN
+// (even) 32-column blocks, the first WN / 2 hold gate columns and the rest
+// the up columns of the same outputs, and the tile writes silu(g) * u,
 // BN / 2 columns of y.
 #pragma once
 #include <type_traits>
@@ -55,20 +55,25 @@ struct TileCfg {
   int WM, WN, GM, GN, ring;
   double quality;  // relative efficiency of the tile shape (operand reuse)
   bool group_ok;   // fits the registers with group-mode accumulators
+  bool plain_ok;   // serves the plain output (its fp32 tile fits the LDS ring)
+  bool gated_ok;   // serves the gated output (an even number of blocks per wave)
 };
 // The weights come from plan sweeps of the layer shapes at M = 256..2048 in
 // both scale modes.  A 64 x 96 tile (two waves) lost to 64 x 64 wherever it
 // was chosen (group qkv at M = 256: 23.4 against 16.4 us) and was dropped.
+// 128 x 256 serves only the gated output: its plain fp32 tile (133 KB)
+// would not fit the 128 KB ring, the gated one (64 KB) does.
 constexpr TileCfg kMenu[] = {
-    {2, 3, 2, 2, 4, 1.00, false},  // 128 x 192, 4 waves
-    {2, 2, 2, 2, 4, 0.95, true},   // 128 x 128, 4 waves
-    {1, 1, 2, 2, 4, 0.80, true},   // 64 x 64, 4 waves
+    {2, 3, 2, 2, 4, 1.00, false, true, false},  // 128 x 192, 4 waves
+    {2, 2, 2, 2, 4, 0.95, true, true, true},    // 128 x 128, 4 waves
+    {1, 1, 2, 2, 4, 0.80, true, true, false},   // 64 x 64, 4 waves
+    {2, 4, 2, 2, 4, 1.05, false, false, true},  // 128 x 256, 4 waves (gated)
 };
 constexpr int kMenuSize = sizeof(kMenu) / sizeof(kMenu[0]);
 
 template <int WM, int WN, int GM, int GN, bool GROUP, int kRing, bool SW>
 __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
-  static_assert(!SW || WN == 2, "gated tiles pair one gate and one up block per wave");
+  static_assert(!SW || WN % 2 == 0, "gated tiles pair gate and up blocks per wave");
   constexpr int kThreads = GM * GN * 64;
   constexpr int kWaves = GM * GN;
   constexpr int BM = 32 * WM * GM, BN = 32 * WN * GN;
@@ -169,8 +174,12 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   // LDS read offsets of this lane's MFMA operands: activation row
   // wm 32 WM + 32 i + l32 (its chunks c sit at c ^ ((row >> 1) & 7)), weight column
   // wn 32 WN + 32 j + l32 of the stage's weight tiles (gated: column
-  // j BN/2 + 32 wn + l32, block 0 in the gate half, block 1 in the up half).
-  auto tile_col = [&](int j) { return SW ? j * (BN / 2) + wn * 32 + l32 : wn * 32 * WN + j * 32 + l32; };
+  // (j >= WN/2) BN/2 + 32 (WN/2) wn + 32 (j mod WN/2) + l32: blocks below
+  // WN/2 in the gate half, the rest in the up half).
+  constexpr int HW = SW ? WN / 2 : WN;  // blocks per wave in each half
+  auto tile_col = [&](int j) {
+    return SW ? (j >= HW ? BN / 2 : 0) + wn * 32 * HW + (j % HW) * 32 + l32 : wn * 32 * WN + j * 32 + l32;
+  };
   const int swz = (l32 >> 1) & 7;
   uint32_t a_rd[WM], b_rd[WN];
 #pragma unroll
@@ -249,7 +258,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   float swv[WN];
 #pragma unroll
   for (int j = 0; j < WN; ++j)
-    swv[j] = SW ? __uint_as_float(buf_load4(j ? wsres_u : wsres, (uint32_t)((wn * 32 + l32) * 4)))
+    swv[j] = SW ? __uint_as_float(buf_load4(j >= HW ? wsres_u : wsres, (uint32_t)((wn * 32 * HW + (j % HW) * 32 + l32) * 4)))
                 : __uint_as_float(buf_load4(wsres, (uint32_t)((wn * 32 * WN + j * 32 + l32) * 4)));
   uint4 sx4[WM][4];
   auto load_sx = [&]() {
@@ -483,12 +492,12 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
       return __fmul_rn(__fmul_rn((float)(acc[0][i][j][r] >> 4), sx), swv[j]);
     }
   };
-  // The output tile: OWN 32-column blocks per wave (gated: one, the
-  // activation of the gate block and the up block).
-  constexpr int OWN = SW ? 1 : WN;
+  // The output tile: OWN 32-column blocks per wave (gated: WN / 2, each the
+  // activation of a gate block and its up block).
+  constexpr int OWN = SW ? WN / 2 : WN;
   auto out_value = [&](int i, int j, int r) -> float {
     if constexpr (SW) {
-      const float g = result(i, 0, r), u = result(i, 1, r);
+      const float g = result(i, j, r), u = result(i, j + OWN, r);
       return __fmul_rn(__fdiv_rn(g, __fadd_rn(1.0f, __expf(-g))), u);
     } else {
       return result(i, j, r);
@@ -569,8 +578,6 @@ template <int C, bool GROUP, bool SW = false>
 constexpr LargeMKernelFn menu_kernel() {
   return largem<kMenu[C].WM, kMenu[C].WN, kMenu[C].GM, kMenu[C].GN, GROUP, kMenu[C].ring, SW>;
 }
-// The tile the gated instances use: 128 x 128, two blocks per wave.
-constexpr int kGatedCfg = 1;
 
 }  // namespace
 

@@ -141,7 +141,9 @@ def test_swiglu_plans_and_rejections():
         assert nt % 2 == 0 and (F // 16) % (nt // 2) == 0, d
     # large M: the 128 x 128 tile, 64 output columns per tile
     d = w.w4a8_linear_swiglu_describe(1024, 24576, 4096)
-    assert "largem<128x128,channel,swiglu>" in d and "tiles=8x192" in d, d
+    assert "largem<128x256,channel,swiglu>" in d and "tiles=8x96" in d, d
+    d = w.w4a8_linear_swiglu_describe(1024, 24576, 4096, 1)
+    assert "largem<128x128,group,swiglu>" in d and "tiles=8x192" in d, d
     assert "largem<128x128,group,swiglu> tiles=1x2" in w.w4a8_linear_swiglu_describe(65, 160, 256, 1)
     assert w.w4a8_linear_swiglu_workspace_bytes(1024, 24576, 4096) == w.w4a8_linear_workspace_bytes(1024, 24576, 4096)
     # shapes the gated call rejects

@@ -110,6 +110,17 @@ def test_gate_up_prefill(group):
     check(1024, 12288, 4096, group, False, 331, "gate+up prefill", rows=rows)
 
 
+def test_wide_gated_tile_ragged():
+    # the 128 x 256 gated tile (128 output columns) with a ragged last row
+    # tile (1000 = 7 x 128 + 104) and a half-full last column tile (12224 =
+    # 95 x 128 + 64); sampled rows include the last row tile
+    M, F, K = 1000, 12224, 4096
+    assert "largem<128x256,channel,swiglu>" in w.w4a8_linear_swiglu_describe(M, 2 * F, K)
+    r = np.random.Generator(np.random.PCG64(344))
+    rows = np.sort(np.concatenate([r.choice(896, 24, replace=False), r.choice(np.arange(896, 1000), 24, replace=False)]))
+    check(M, F, K, False, False, 345, "wide gated tile", rows=rows)
+
+
 @pytest.mark.parametrize("group", [False, True])
 @pytest.mark.parametrize("M,F,K,codes,seed", [
     (65, 48, 256, False, 340),     # just past the small-M path; one ragged 64-column tile

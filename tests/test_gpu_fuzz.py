@@ -52,3 +52,32 @@ def test_random_shape(M, K, N, group, codes, seed):
     W, s = I.weights(N, K, seed + 1, group=group)
     check_all_outputs(x, W, s, group=group, codes=codes,
                       label=f"fuzz {w.w4a8_linear_describe(M, N, K, int(group), int(codes)).split(' workspace')[0][:40]}")
+
+
+def gated_cases(seed=20260913):
+    """Gated gate+up shapes: small M (any even tile count), K splits, and
+    large M over both gated tiles (F = N / 2 any multiple of 16)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    any_codes = lambda: bool(rng.integers(0, 2))
+    strata = [
+        (8, lambda: (int(rng.integers(1, 65)), 128 * int(rng.integers(1, 97)), 16 * int(rng.integers(1, 769)))),
+        (3, lambda: (int(rng.integers(1, 17)), 128 * int(rng.integers(256, 513)), 16 * int(rng.integers(1, 3)))),
+        (7, lambda: (int(rng.integers(65, 2100)), 128 * int(rng.integers(1, 33)), 16 * int(rng.integers(4, 769)))),
+    ]
+    out = []
+    for n, draw in strata:
+        got = 0
+        while got < n:
+            M, K, F = draw()
+            if M * 2 * F * K > MAX_MACS:
+                continue
+            out.append((M, K, F, bool(rng.integers(0, 2)), any_codes(), int(rng.integers(1 << 30))))
+            got += 1
+    return out
+
+
+@pytest.mark.parametrize("M,K,F,group,codes,seed", gated_cases())
+def test_random_gated_shape(M, K, F, group, codes, seed):
+    from test_gpu_swiglu import check
+    check(M, F, K, group, codes, seed,
+          f"fuzz {w.w4a8_linear_swiglu_describe(M, 2 * F, K, int(group), int(codes)).split(' workspace')[0][:40]}")

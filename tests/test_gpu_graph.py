@@ -59,3 +59,44 @@ def test_graph_replays_match_eager(M, group):
         torch.cuda.synchronize()
         for i, c in enumerate(calls):
             assert torch.equal(c[4].view(torch.int16), ref[i].view(torch.int16)), ("eager", rep, i)
+
+
+@pytest.mark.parametrize("M,F,K,group", [(16, 12288, 4096, False), (16, 16, 65536, True), (1024, 12288, 4096, False)])
+def test_gated_graph_replays_match_eager(M, F, K, group):
+    # the gated gate+up call: small M, small M with K split (its arrival
+    # counters are reset by every call), and the large-M gated tile
+    dev = torch.device("cuda:0")
+    mode = w.SCALE_GROUP_F16 if group else w.SCALE_CHANNEL_F32
+    print(f"[case] gated graph M={M} F={F} K={K} group={group} "
+          f"plan={w.w4a8_linear_swiglu_describe(M, 2 * F, K, mode, 0)}", flush=True)
+    W, s = I.weights(2 * F, K, 3000 + M, group=group)
+    wp = w.w4a8_pack_weights(torch.from_numpy(W).to(dev))
+    sd = torch.from_numpy(s).to(dev)
+    x = torch.from_numpy(I.activations(M, K, 3001 + M).view(np.int16)).to(dev).view(torch.bfloat16)
+    y = torch.empty((M, F), dtype=torch.bfloat16, device=dev)
+    ws = w.Workspace(dev)
+    ws.get(w.w4a8_linear_swiglu_workspace_bytes(M, 2 * F, K, mode))
+
+    def call(stream=None):
+        w.w4a8_linear_swiglu(x, wp, sd, 2 * F, scale_mode=mode, out=y, workspace=ws, stream=stream)
+
+    call()
+    torch.cuda.synchronize()
+    ref = y.clone()
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            call(stream=cap)
+            call(stream=cap)
+    torch.cuda.current_stream().wait_stream(cap)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        y.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), ref.view(torch.int16)), rep
+        call()
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), ref.view(torch.int16)), ("eager", rep)

@@ -158,3 +158,51 @@ def gated(out):
     g32, u32 = out["y32"][:, :F], out["y32"][:, F:]
     return dict(y64=silu_mul(g64, u64), y_of32=silu_mul(g32, u32), g64=g64, u64=u64,
                 g_bound=out["bound"][:, :F], u_bound=out["bound"][:, F:])
+
+
+def rmsnorm_quantize(x_bits, gamma_bits, eps):
+    """RMSNorm of each token row followed by the per-token int8 quantize,
+    the normalization prologue of a backbone linear.
+
+    FlashDrive Sec. 3.5 (Kernel Fusion) merges consecutive element-wise and
+    reduction operations with the GEMMs without naming them; RMSNorm with a
+    learned bf16 gain is this oracle's reading of the normalization.  Per
+    row (fp32 IEEE operations unless stated):
+        ss = sum_k x_k^2               (exact squares; math.fsum, fp64)
+        v  = fl32(ss / K)              (fp64 division, then rounded to fp32)
+        r  = 1 / sqrt(v + eps)
+        h_k = (x_k * r) * gamma_k
+    then the quantize of quantize_act on the fp32 h: a = max_k |h_k|,
+    s = a / 127, q_k = round_half_even(h_k / s) clamped to [-127, 127]; an
+    all-zero h has s = 0 and q = 0.  Inputs must be finite, eps > 0 (so r is
+    finite) and fl32(ss / K) finite; |h_k| <= sqrt(K) |gamma_k| then holds.
+    Returns (q int8 [M][K], s fp32 [M], h fp32 [M][K], r fp32 [M]).
+    """
+    import math
+
+    x = (np.ascontiguousarray(x_bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+    g = (np.ascontiguousarray(gamma_bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+    if not (np.isfinite(x).all() and np.isfinite(g).all() and math.isfinite(eps) and np.float32(eps) > 0):
+        raise ValueError("rmsnorm_quantize takes finite inputs and eps > 0")
+    M, K = x.shape
+    assert g.shape == (K,)
+    e32 = np.float32(eps)
+    q = np.zeros((M, K), np.int8)
+    s = np.zeros(M, np.float32)
+    h = np.empty((M, K), np.float32)
+    r = np.empty(M, np.float32)
+    for m in range(M):
+        x64 = x[m].astype(np.float64)
+        ss = math.fsum(x64 * x64)              # each square is exact in fp64
+        v = np.float32(ss / K)
+        if not np.isfinite(v):
+            raise ValueError("rmsnorm_quantize: mean square beyond the fp32 range")
+        rr = np.float32(1.0) / np.sqrt(np.float32(v + e32))
+        r[m] = rr
+        h[m] = (x[m] * rr) * g
+        a = np.float32(np.max(np.abs(h[m])))
+        if a == 0:
+            continue
+        s[m] = a / np.float32(127.0)
+        q[m] = np.clip(np.rint(h[m] / s[m]), -127, 127).astype(np.int8)
+    return q, s, h, r

@@ -388,3 +388,90 @@ def test_gated_output_halves_and_composition():
     # a zero gate gives an exactly zero output whatever the up projection
     zero = oracle.gated(oracle.linear(x, np.concatenate([np.zeros_like(Wg), Wu]), s_w=s))
     assert not zero["y64"].any() and not zero["y_of32"].any()
+
+
+# ---------------------------------------------------------------- norm + quantize prologue
+
+def test_rmsnorm_power_of_two_rows_reduce_to_the_quantize_of_gamma():
+    # x_k = c = +-2^j, eps tiny: ss = K c^2, v = c^2, r = 1/|c| (every step
+    # exact), so h = sign(c) gamma and the codes are quantize_act(gamma)'s
+    K = 384
+    g = I.activations(1, K, 95)[0]
+    for c in (1.0, -4.0, 2.0 ** -10, 2.0 ** 12):
+        x = bits_of(np.full((1, K), c))
+        q, s, h, r = oracle.rmsnorm_quantize(x, g, 2.0 ** -126)
+        qg, sg = oracle.quantize_act(g[None, :])
+        assert r[0] == np.float32(1.0 / abs(c))
+        np.testing.assert_array_equal(h[0], np.sign(c) * f32_of_bits(g))
+        np.testing.assert_array_equal(q[0], np.sign(c).astype(np.int8) * qg[0])
+        assert s[0] == sg[0]
+
+
+def test_rmsnorm_known_mean_square_and_eps():
+    # a quarter of the entries +-2, the rest 0: mean square exactly 1.  With
+    # gamma = 1 and eps tiny, r = 1 and the codes are quantize_act(x)'s; with
+    # eps = 3, r = 1/2 exactly and the scale halves (eps goes with the mean,
+    # under the root)
+    K = 512
+    r_ = rng(96)
+    vals = np.zeros((3, K), np.float32)
+    for m in range(3):
+        idx = r_.permutation(K)[: K // 4]
+        vals[m, idx] = r_.choice([-2.0, 2.0], size=K // 4)
+    x = bits_of(vals)
+    one = bits_of(np.ones(K))
+    q0, s0 = oracle.quantize_act(x)
+    q, s, h, r = oracle.rmsnorm_quantize(x, one, 2.0 ** -126)
+    assert (r == 1.0).all()
+    np.testing.assert_array_equal(q, q0)
+    np.testing.assert_array_equal(s, s0)
+    q, s, h, r = oracle.rmsnorm_quantize(x, one, 3.0)
+    assert (r == 0.5).all()
+    np.testing.assert_array_equal(q, q0)
+    np.testing.assert_array_equal(s, s0 * np.float32(0.5))
+
+
+def test_rmsnorm_scale_invariance():
+    # x -> 2^j x leaves h unchanged when eps is negligible against the mean
+    # square (a wrong power in the root, or a missing one, would not)
+    K = 1024
+    x = I.activations(4, K, 97)
+    g = I.activations(1, K, 98)[0]
+    xf = f32_of_bits(x)
+    q1, s1, h1, _ = oracle.rmsnorm_quantize(x, g, 2.0 ** -126)
+    for j in (-3, 5):
+        q2, s2, h2, _ = oracle.rmsnorm_quantize(bits_of(xf * np.float32(2.0 ** j)), g, 2.0 ** -126)
+        np.testing.assert_array_equal(h1, h2)
+        np.testing.assert_array_equal(q1, q2)
+        np.testing.assert_array_equal(s1, s2)
+
+
+def test_rmsnorm_matches_float64_definition():
+    # fp64 reference of the same formula: r within 2 ulp (fp32), codes within
+    # one step where the fp32 quotient sits next to a half
+    K = 2048
+    x = I.activations(8, K, 99)
+    g = I.activations(1, K, 100)[0]
+    q, s, h, r = oracle.rmsnorm_quantize(x, g, 1e-6)
+    xf = f32_of_bits(x).astype(np.float64)
+    r64 = 1.0 / np.sqrt((xf * xf).mean(axis=1) + np.float64(np.float32(1e-6)))
+    np.testing.assert_allclose(r, r64, rtol=2.5e-7)
+    h64 = xf * r64[:, None] * f32_of_bits(g).astype(np.float64)
+    np.testing.assert_allclose(h, h64, rtol=5e-7, atol=1e-30)
+    q64 = h64 / (np.abs(h64).max(axis=1, keepdims=True) / 127.0)
+    assert np.abs(q.astype(np.float64) - q64).max() <= 0.5 + 1e-4
+
+
+def test_rmsnorm_zero_row_and_rejections():
+    K = 256
+    x = np.zeros((2, K), np.uint16)
+    x[1] = I.activations(1, K, 101)[0]
+    g = bits_of(np.ones(K))
+    q, s, h, r = oracle.rmsnorm_quantize(x, g, 1e-6)
+    assert s[0] == 0 and not q[0].any() and not h[0].any()
+    with pytest.raises(ValueError):
+        oracle.rmsnorm_quantize(x, g, 0.0)
+    bad = x.copy()
+    bad[1, 3] = 0x7F80  # +inf
+    with pytest.raises(ValueError):
+        oracle.rmsnorm_quantize(bad, g, 1e-6)

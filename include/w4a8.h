@@ -118,6 +118,34 @@ w4a8_status w4a8_quantize_act(const uint16_t* x, int64_t M, int64_t K, int8_t* x
                               float* x_scale, hipStream_t stream);
 
 /*
+ * The normalization prologue of a backbone linear: RMSNorm of each token row,
+ * then the per-token quantize of w4a8_quantize_act applied to the fp32
+ * normalized row, in one kernel.  FlashDrive, Sec. 3.5 ("Kernel Fusion"),
+ * merges consecutive element-wise and reduction operations with the GEMMs
+ * without naming them; RMSNorm with a learned gain is this library's
+ * reading of the normalization in front of the QKV and gate+up projections.
+ * Per row m, with fp32 IEEE operations unless stated:
+ *     ss = sum_k x[m,k]^2      (fp64, every square exact; any summation order)
+ *     v  = fl32(ss / K)        (fp64 division rounded to fp32)
+ *     r  = 1 / sqrt(v + eps)
+ *     h[m,k] = (x[m,k] * r) * gamma[k]
+ *     x_scale[m] = max_k |h[m,k]| / 127,
+ *     x_q[m,k] = round_half_even(h[m,k] / x_scale[m])   (0 for an all-zero row)
+ * The output feeds w4a8_linear / w4a8_linear_swiglu as W4A8_IN_I8.
+ *   x        device, bf16 bit patterns [M][K], finite, 16-byte aligned
+ *   gamma    device, bf16 gain [K], finite, 16-byte aligned
+ *   eps      0 < eps < inf (W4A8_EINVAL otherwise); fl32(ss / K) must be finite
+ *   M, K     0 <= M <= W4A8_M_MAX (0 is a no-op), K % 128 == 0, 128 <= K <= W4A8_K_MAX
+ *   x_q      device, int8 [M][K], 16-byte aligned
+ *   x_scale  device, fp32 [M], 4-byte aligned
+ * Does not synchronize.  The fp64 sum is reduced in a fixed order, so a call
+ * is deterministic; a different order can change v only where ss / K lies
+ * within a few fp64 ulps of an fp32 rounding boundary.
+ */
+w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, float eps, int64_t M, int64_t K,
+                                      int8_t* x_q, float* x_scale, hipStream_t stream);
+
+/*
  * Bytes of device workspace w4a8_linear needs for this problem (0 if none).
  * The workspace holds split-K partial sums and arrival counters (and, when
  * bf16 input is quantized by its own kernel, the int8 codes and scales).

@@ -26,7 +26,7 @@ GROUP_SIZE = 128
 EXPORTS = ("w4a8_status_string", "w4a8_packed_weight_bytes", "w4a8_pack_weights",
            "w4a8_quantize_act", "w4a8_linear_workspace_bytes", "w4a8_linear",
            "w4a8_linear_describe", "w4a8_linear_swiglu", "w4a8_linear_swiglu_workspace_bytes",
-           "w4a8_linear_swiglu_describe")
+           "w4a8_linear_swiglu_describe", "w4a8_rmsnorm_quantize_act")
 
 _OUT_DTYPE = {OUT_BF16: torch.bfloat16, OUT_F32: torch.float32, OUT_I32_ACC: torch.int32}
 
@@ -57,6 +57,8 @@ def lib() -> ctypes.CDLL:
         L.w4a8_pack_weights.restype = I
         L.w4a8_quantize_act.argtypes = [P, I64, I64, P, P, P]
         L.w4a8_quantize_act.restype = I
+        L.w4a8_rmsnorm_quantize_act.argtypes = [P, P, ctypes.c_float, I64, I64, P, P, P]
+        L.w4a8_rmsnorm_quantize_act.restype = I
         L.w4a8_linear_workspace_bytes.argtypes = [I64, I64, I64, I, I]
         L.w4a8_linear_workspace_bytes.restype = SZ
         L.w4a8_linear.argtypes = [P, I, P, I64, I64, P, P, I, I64, P, I, P, SZ, P]
@@ -125,6 +127,22 @@ def w4a8_quantize_act(x: torch.Tensor, stream=None):
     rc = lib().w4a8_quantize_act(_dev(x, "x", torch.bfloat16), M, K, _dev(q, "q", torch.int8),
                                  _dev(s, "s", torch.float32), _stream(stream))
     _check(rc, "w4a8_quantize_act")
+    return q, s
+
+
+def w4a8_rmsnorm_quantize_act(x: torch.Tensor, gamma: torch.Tensor, eps: float, stream=None):
+    """RMSNorm (gain gamma bf16 [K], eps > 0) of bf16 x [M][K] then the
+    per-token int8 quantize of the fp32 result -> (codes int8 [M][K],
+    scales fp32 [M]), the int8 input of w4a8_linear."""
+    M, K = x.shape
+    x_ptr = _dev(x, "x", torch.bfloat16)
+    g_ptr = _dev(gamma, "gamma", torch.bfloat16)
+    if tuple(gamma.shape) != (K,):
+        raise ValueError(f"gamma must be [{K}]")
+    q = torch.empty((M, K), dtype=torch.int8, device=x.device)
+    s = torch.empty((M,), dtype=torch.float32, device=x.device)
+    rc = lib().w4a8_rmsnorm_quantize_act(x_ptr, g_ptr, float(eps), M, K, q.data_ptr(), s.data_ptr(), _stream(stream))
+    _check(rc, "w4a8_rmsnorm_quantize_act")
     return q, s
 
 

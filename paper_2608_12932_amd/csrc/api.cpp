@@ -215,6 +215,19 @@ w4a8_status w4a8_quantize_act(const uint16_t* x, int64_t M, int64_t K, int8_t* x
   return launch_quantize(x, (int)M, (int)K, x_q, x_scale, stream) == hipSuccess ? W4A8_OK : W4A8_EHIP;
 }
 
+w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, float eps, int64_t M, int64_t K,
+                                      int8_t* x_q, float* x_scale, hipStream_t stream) {
+  if (M < 0 || M > W4A8_M_MAX) return W4A8_EINVAL;
+  if (K < W4A8_GROUP_SIZE || K % W4A8_GROUP_SIZE || K > W4A8_K_MAX) return W4A8_EINVAL;
+  if (!(eps > 0.0f) || !(eps <= 3.4e38f)) return W4A8_EINVAL;  // also rejects NaN and inf
+  if (M == 0) return W4A8_OK;
+  if (!x || !gamma || !x_q || !x_scale || !aligned(x, 16) || !aligned(gamma, 16) || !aligned(x_q, 16) ||
+      !aligned(x_scale, 4))
+    return W4A8_EINVAL;
+  return launch_rmsnorm_quantize(x, gamma, eps, (int)M, (int)K, x_q, x_scale, stream) == hipSuccess ? W4A8_OK
+                                                                                                  : W4A8_EHIP;
+}
+
 size_t w4a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind) {
   return workspace_bytes(M, N, K, scale_mode, in_kind, false);
 }

@@ -12,6 +12,9 @@ enum OutKind { kOutBF16 = 0, kOutF32 = 1, kOutI32 = 2 };
 // ---- activation quantize (quantize.hip)
 hipError_t launch_quantize(const uint16_t* x, int M, int K, int8_t* q, float* scale,
                            hipStream_t stream);
+// RMSNorm (gain gamma, eps > 0) of each row, then the quantize of the fp32 result
+hipError_t launch_rmsnorm_quantize(const uint16_t* x, const uint16_t* gamma, float eps, int M, int K, int8_t* q,
+                                   float* scale, hipStream_t stream);
 
 // ---- weight pack (pack.hip); `err` is a device word set to 1 on a range error
 hipError_t launch_pack(const int8_t* w, int N, int K, uint8_t* out, unsigned* err,

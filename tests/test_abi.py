@@ -158,3 +158,16 @@ def test_swiglu_plans_and_rejections():
     assert f(fake, 0, None, 4, 256, fake, fake, 0, 256, fake, w.OUT_I32_ACC, None, 0, None) == w.W4A8_EINVAL
     assert f(None, 0, None, 0, 256, None, None, 0, 256, None, 0, None, 0, None) == w.W4A8_OK
     assert f(None, 0, None, 4, 256, fake, fake, 0, 256, fake, 0, None, 0, None) == w.W4A8_EINVAL
+
+
+def test_rmsnorm_quantize_rejections():
+    L = w.lib()
+    P = ctypes.c_void_p
+    fake = P(1 << 20)
+    f = L.w4a8_rmsnorm_quantize_act
+    assert f(fake, fake, 0.0, 4, 256, fake, fake, None) == w.W4A8_EINVAL       # eps must be > 0
+    assert f(fake, fake, float("nan"), 4, 256, fake, fake, None) == w.W4A8_EINVAL
+    assert f(fake, fake, 1e-6, 4, 200, fake, fake, None) == w.W4A8_EINVAL      # K % 128
+    assert f(None, fake, 1e-6, 4, 256, fake, fake, None) == w.W4A8_EINVAL
+    assert f(fake, P((1 << 20) + 8), 1e-6, 4, 256, fake, fake, None) == w.W4A8_EINVAL  # misaligned gamma
+    assert f(None, None, 1e-6, 0, 256, None, None, None) == w.W4A8_OK          # M == 0 is a no-op

@@ -327,6 +327,61 @@ def bench_gate_up_swiglu(steps, warmup, copies=16):
             "weight_copies": copies, "unfused": "w4a8_linear bf16 [M][N], then torch silu and mul", "rows": rows}
 
 
+def bench_rmsnorm_prologue(steps):
+    """The normalization prologue of the gate+up projection (K = 4096) at M =
+    16 and 1024, graph-replayed: w4a8_rmsnorm_quantize_act (one kernel)
+    against torch's RMSNorm in fp32 rounded to bf16, then
+    w4a8_quantize_act; and each prologue followed by the gate+up GEMM on
+    its int8 codes (N = 24576, per-channel scales)."""
+    import torch
+    import paper_2608_12932_amd as w
+    from paper_2608_12932_amd import inputs as I
+
+    L = w.lib()
+    rows, cache = [], {}
+    for M in (16, 1024):
+        xd, wps, sd, y, K, N, sbytes = _dev_inputs("gate_up_verify", M, 0, 8, cache)
+        gamma = torch.from_numpy(I.activations(1, K, 77, outliers=False)[0].view(np.int16)).to(xd.device).view(torch.bfloat16)
+        q = torch.empty((M, K), dtype=torch.int8, device=xd.device)
+        sx = torch.empty((M,), dtype=torch.float32, device=xd.device)
+        xp, gp, qp, sp = xd.data_ptr(), gamma.data_ptr(), q.data_ptr(), sx.data_ptr()
+        gf = gamma.float()
+        hb = torch.empty_like(xd)
+        hp = hb.data_ptr()
+
+        def fused(i, stream):
+            L.w4a8_rmsnorm_quantize_act(xp, gp, 1e-6, M, K, qp, sp, stream)
+
+        def unfused(i, stream):
+            xf = xd.float()
+            hb.copy_(xf * torch.rsqrt(xf.pow(2).mean(-1, keepdim=True) + 1e-6) * gf)
+            L.w4a8_quantize_act(hp, M, K, qp, sp, stream)
+
+        gemm = DirectCall(q, wps, sd, N, y, x_scale=sx)
+
+        def fused_gemm(i, stream):
+            fused(i, stream)
+            gemm(i, stream)
+
+        def unfused_gemm(i, stream):
+            unfused(i, stream)
+            gemm(i, stream)
+
+        t = {k: graph_ms(f, steps) * 1e3 for k, f in (("fused", fused), ("unfused", unfused),
+                                                       ("fused_gemm", fused_gemm), ("unfused_gemm", unfused_gemm))}
+        nbytes = M * K * 2 + K * 2 + M * K + M * 4
+        rows.append({"M": M, "us_fused": round(t["fused"], 3), "us_unfused": round(t["unfused"], 3),
+                     "GB/s_fused": round(nbytes / (t["fused"] * 1e-6) / 1e9, 1),
+                     "us_fused_with_gemm": round(t["fused_gemm"], 3), "us_unfused_with_gemm": round(t["unfused_gemm"], 3),
+                     "algorithmic_bytes": nbytes})
+        del xd, wps, sd, y, q, sx, gemm
+    cache.clear()
+    torch.cuda.empty_cache()
+    return {"workload": "RMSNorm + int8 quantize prologue of the gate+up projection (K = 4096), graph-replayed",
+            "unfused": "torch RMSNorm (fp32, rounded to bf16) then w4a8_quantize_act",
+            "gemm": "gate+up N = 24576 on the int8 codes, per-channel scales", "rows": rows}
+
+
 def bench_layer_group(steps, warmup, copies=6):
     """One decoder layer's four linears (QKV, O, gate+up, down) with group-128
     fp16 scales; a step is the four calls, each on its own bf16 x.  Six copies
@@ -508,6 +563,7 @@ def main():
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
         print(json.dumps({"sweep": {"down_verify": bench_down_verify(ss, sw),
                                     "gate_up_swiglu": bench_gate_up_swiglu(ss, sw),
+                                    "rmsnorm_prologue": bench_rmsnorm_prologue(ss),
                                     "layer_group": bench_layer_group(ss, sw),
                                     "stack": bench_stack(max(10, args.steps // 50))}}), flush=True)
         return
@@ -561,6 +617,7 @@ def main():
     if not args.no_sweep:
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
         out["sweep"] = {"down_verify": bench_down_verify(ss, sw), "gate_up_swiglu": bench_gate_up_swiglu(ss, sw),
+                        "rmsnorm_prologue": bench_rmsnorm_prologue(ss),
                         "layer_group": bench_layer_group(ss, sw),
                         "stack": bench_stack(max(10, args.steps // 50))}
     if not args.no_cpu_baseline:

@@ -121,8 +121,8 @@ w4a8_status w4a8_quantize_act(const uint16_t* x, int64_t M, int64_t K, int8_t* x
  * The normalization prologue of a backbone linear: RMSNorm of each token row,
  * then the per-token quantize of w4a8_quantize_act applied to the fp32
  * normalized row, in one kernel.  FlashDrive, Sec. 3.5 ("Kernel Fusion"),
- * merges consecutive element-wise and reduction operations with the GEMMs
- * without naming them; RMSNorm with a learned gain is this library's
+ * folds the pointwise and row-reduction work around the GEMMs into them,
+ * without saying which ops those are; RMSNorm with a learned gain is this library's
  * reading of the normalization in front of the QKV and gate+up projections.
  * Per row m, with fp32 IEEE operations unless stated:
  *     ss = sum_k x[m,k]^2      (fp64, every square exact; any summation order)

@@ -164,9 +164,10 @@ def rmsnorm_quantize(x_bits, gamma_bits, eps):
     """RMSNorm of each token row followed by the per-token int8 quantize,
     the normalization prologue of a backbone linear.
 
-    FlashDrive Sec. 3.5 (Kernel Fusion) merges consecutive element-wise and
-    reduction operations with the GEMMs without naming them; RMSNorm with a
-    learned bf16 gain is this oracle's reading of the normalization.  Per
+    FlashDrive Sec. 3.5 (Kernel Fusion) folds the pointwise and row-reduction
+    work around its GEMMs into them, without saying which ops those are;
+    RMSNorm with a learned bf16 gain is this oracle's reading of the
+    normalization.  Per
     row (fp32 IEEE operations unless stated):
         ss = sum_k x_k^2               (exact squares; math.fsum, fp64)
         v  = fl32(ss / K)              (fp64 division, then rounded to fp32)

@@ -207,3 +207,78 @@ def rmsnorm_quantize(x_bits, gamma_bits, eps):
         s[m] = a / np.float32(127.0)
         q[m] = np.clip(np.rint(h[m] / s[m]), -127, 127).astype(np.int8)
     return q, s, h, r
+
+
+def _bf16_round(x32):
+    """fp32 -> bf16 bit patterns, round to nearest even (finite inputs)."""
+    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def _f32(bits):
+    return (np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def rope_rotate(x_bits, pos, cos_t, sin_t):
+    """Rotary embedding of bf16 rows x [N][D] at integer positions pos [N],
+    rotate-half pairing (d, d + D/2), angles given by the caller's fp32
+    tables cos_t, sin_t [P][D/2]; fp32 IEEE operations, result rounded to
+    bf16 (the rotated operands of a bf16 model):
+        y_i       = x_i cos - x_{i+D/2} sin
+        y_{i+D/2} = x_{i+D/2} cos + x_i sin
+    Returns bf16 bit patterns [N][D]."""
+    x = _f32(x_bits)
+    D = x.shape[1]
+    h = D // 2
+    c = cos_t[pos].astype(np.float32)
+    s = sin_t[pos].astype(np.float32)
+    a, b = x[:, :h], x[:, h:]
+    y = np.empty_like(x)
+    y[:, :h] = (a * c) - (b * s)
+    y[:, h:] = (b * c) + (a * s)
+    return _bf16_round(y)
+
+
+def streaming_attention(q_bits, k_bits, v_bits, pos_q, pos_k, cos_t, sin_t, scale):
+    """Streaming prefill attention (FlashDrive Sec. 3.1, streaming design):
+    queries are the newest frame's tokens, keys and values the whole
+    window's cache, keys stored before their rotary embedding and rotated
+    here at their current window positions; the streaming mask lets query
+    i see key j iff pos_k[j] <= pos_q[i] (causal order of the view-major
+    window).
+
+    q [H][Nq][D], k and v [Hkv][Nk][D] bf16 bit patterns (query head h reads
+    kv head h // (H / Hkv)); pos_q [Nq], pos_k [Nk] int; tables [P][D/2]
+    fp32.  Rotated q and k are rounded to bf16 (rope_rotate); scores,
+    softmax and the weighted sum are fp64.  Returns (o64 [H][Nq][D] fp64,
+    bnd [H][Nq][D] fp64 = sum_j P_ij |v_jd|, the cancellation-free size of
+    each output)."""
+    H, Nq, D = q_bits.shape
+    Hkv, Nk, _ = k_bits.shape
+    G = H // Hkv
+    pos_q = np.asarray(pos_q)
+    pos_k = np.asarray(pos_k)
+    vis = pos_k[None, :] <= pos_q[:, None]                     # [Nq][Nk]
+    if not vis.any(axis=1).all():
+        raise ValueError("every query must see at least one key")
+    o64 = np.empty((H, Nq, D))
+    bnd = np.empty((H, Nq, D))
+    kr = [_f32(rope_rotate(k_bits[g], pos_k, cos_t, sin_t)).astype(np.float64) for g in range(Hkv)]
+    vv = [_f32(v_bits[g]).astype(np.float64) for g in range(Hkv)]
+    for h in range(H):
+        qr = _f32(rope_rotate(q_bits[h], pos_q, cos_t, sin_t)).astype(np.float64)
+        s = (qr @ kr[h // G].T) * float(scale)
+        s = np.where(vis, s, -np.inf)
+        s -= s.max(axis=1, keepdims=True)
+        p = np.exp(s)
+        p /= p.sum(axis=1, keepdims=True)
+        o64[h] = p @ vv[h // G]
+        bnd[h] = p @ np.abs(vv[h // G])
+    return o64, bnd
+
+
+def rope_tables(P, D, base=10000.0):
+    """fp32 cos / sin tables [P][D/2] for angle p * base^(-2i/D), from fp64."""
+    i = np.arange(D // 2, dtype=np.float64)
+    ang = np.arange(P, dtype=np.float64)[:, None] * base ** (-2.0 * i / D)[None, :]
+    return np.cos(ang).astype(np.float32), np.sin(ang).astype(np.float32)

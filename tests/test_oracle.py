@@ -475,3 +475,100 @@ def test_rmsnorm_zero_row_and_rejections():
     bad[1, 3] = 0x7F80  # +inf
     with pytest.raises(ValueError):
         oracle.rmsnorm_quantize(bad, g, 1e-6)
+
+
+# ---------------------------------------------------------------- streaming attention
+
+def _attn_inputs(H, Hkv, Nq, Nk, D, seed):
+    q = I.activations(H * Nq, D, seed).reshape(H, Nq, D)
+    k = I.activations(Hkv * Nk, D, seed + 1).reshape(Hkv, Nk, D)
+    v = I.activations(Hkv * Nk, D, seed + 2).reshape(Hkv, Nk, D)
+    return q, k, v
+
+
+def test_rope_rotation_pair_formula_and_norm():
+    # rotate-half pairs (i, i + D/2) by the table's angle: a 90 degree turn
+    # maps (a, b) to (-b, a); any angle keeps the pair's norm (fp32 + bf16)
+    D = 128
+    x = I.activations(6, D, 110)
+    cos_t = np.zeros((3, D // 2), np.float32)
+    sin_t = np.zeros((3, D // 2), np.float32)
+    cos_t[0], sin_t[1] = 1.0, 1.0           # position 0: identity; 1: +90 degrees
+    cos_t[2], sin_t[2] = np.cos(0.7), np.sin(0.7)
+    xf = f32_of_bits(x)
+    y0 = f32_of_bits(oracle.rope_rotate(x, np.zeros(6, int), cos_t, sin_t))
+    y1 = f32_of_bits(oracle.rope_rotate(x, np.ones(6, int), cos_t, sin_t))
+    np.testing.assert_array_equal(y0, xf)
+    np.testing.assert_array_equal(y1[:, : D // 2], -xf[:, D // 2:])
+    np.testing.assert_array_equal(y1[:, D // 2:], xf[:, : D // 2])
+    y2 = f32_of_bits(oracle.rope_rotate(x, np.full(6, 2), cos_t, sin_t)).astype(np.float64)
+    n_in = np.hypot(xf[:, : D // 2], xf[:, D // 2:])
+    n_out = np.hypot(y2[:, : D // 2], y2[:, D // 2:])
+    np.testing.assert_allclose(n_out, n_in, rtol=2 ** -7)
+
+
+def test_rope_scores_depend_on_relative_position():
+    # with exact angles, q(p + d) . k(p' + d) = q(p) . k(p'): shifting every
+    # position by the same amount (the streaming window's shift) keeps the
+    # scores up to the bf16 rounding of the rotated operands
+    D = 128
+    cos_t, sin_t = oracle.rope_tables(4096, D)
+    q = I.activations(1, D, 111, outliers=False)
+    k = I.activations(1, D, 112, outliers=False)
+    def score(pq, pk):
+        a = f32_of_bits(oracle.rope_rotate(q, np.array([pq]), cos_t, sin_t)).astype(np.float64)
+        b = f32_of_bits(oracle.rope_rotate(k, np.array([pk]), cos_t, sin_t)).astype(np.float64)
+        return float((a @ b.T)[0, 0])
+    mag = float((np.abs(f32_of_bits(q)).astype(np.float64) @ np.abs(f32_of_bits(k)).astype(np.float64).T)[0, 0])
+    for pq, pk, d in [(100, 37, 1000), (7, 7, 3000), (500, 0, 64)]:
+        assert abs(score(pq, pk) - score(pq + d, pk + d)) <= 2 ** -6 * mag
+    assert abs(score(100, 37) - score(100, 38)) > 2 ** -6 * mag  # and it does depend on the offset
+
+
+def test_attention_without_rotation_or_mask_is_plain_softmax():
+    # identity tables and equal positions: every key visible, no rotation ->
+    # softmax(q k^T s) v with scipy's softmax
+    import scipy.special
+    H, Hkv, Nq, Nk, D = 4, 2, 5, 24, 128
+    q, k, v = _attn_inputs(H, Hkv, Nq, Nk, D, 113)
+    cos_t = np.ones((1, D // 2), np.float32)
+    sin_t = np.zeros((1, D // 2), np.float32)
+    o, _ = oracle.streaming_attention(q, k, v, np.zeros(Nq, int), np.zeros(Nk, int), cos_t, sin_t, 0.125)
+    for h in range(H):
+        qf = f32_of_bits(q[h]).astype(np.float64)
+        kf = f32_of_bits(k[h // 2]).astype(np.float64)
+        vf = f32_of_bits(v[h // 2]).astype(np.float64)
+        ref = scipy.special.softmax(qf @ kf.T * 0.125, axis=1) @ vf
+        np.testing.assert_allclose(o[h], ref, rtol=1e-12, atol=1e-12)
+
+
+def test_streaming_mask_hides_later_keys():
+    # query i sees key j iff pos_k[j] <= pos_q[i]: values of hidden keys do
+    # not matter; one visible key gives exactly its value; permuting key
+    # slots together with their positions changes nothing
+    H, Hkv, Nq, Nk, D = 2, 1, 4, 16, 128
+    q, k, v = _attn_inputs(H, Hkv, Nq, Nk, D, 114)
+    cos_t, sin_t = oracle.rope_tables(64, D)
+    pos_k = np.arange(Nk) + 10
+    pos_q = np.array([10, 13, 20, 25])
+    o, _ = oracle.streaming_attention(q, k, v, pos_q, pos_k, cos_t, sin_t, 0.1)
+    v2 = v.copy()
+    v2[:, pos_k > 20] = I.activations(int((pos_k > 20).sum()), D, 115)
+    o2, _ = oracle.streaming_attention(q, k, v2, pos_q, pos_k, cos_t, sin_t, 0.1)
+    np.testing.assert_array_equal(o2[:, :3], o[:, :3])   # queries at 10, 13, 20 see none of them
+    assert not np.array_equal(o2[:, 3], o[:, 3])
+    np.testing.assert_array_equal(o[:, 0], np.broadcast_to(f32_of_bits(v[0, 0]).astype(np.float64), (H, D)))
+    perm = rng(116).permutation(Nk)
+    o3, _ = oracle.streaming_attention(q, k[:, perm], v[:, perm], pos_q, pos_k[perm], cos_t, sin_t, 0.1)
+    np.testing.assert_allclose(o3, o, rtol=1e-12, atol=1e-12)
+
+
+def test_attention_of_constant_values_is_that_value():
+    H, Hkv, Nq, Nk, D = 2, 2, 3, 20, 128
+    q, k, _ = _attn_inputs(H, Hkv, Nq, Nk, D, 117)
+    row = I.activations(1, D, 118)[0]
+    v = np.broadcast_to(row, (Hkv, Nk, D)).copy()
+    cos_t, sin_t = oracle.rope_tables(64, D)
+    o, bnd = oracle.streaming_attention(q, k, v, np.array([5, 12, 19]), np.arange(Nk), cos_t, sin_t, 0.3)
+    np.testing.assert_allclose(o, np.broadcast_to(f32_of_bits(row).astype(np.float64), o.shape), rtol=1e-13)
+    np.testing.assert_allclose(bnd, np.abs(o), rtol=1e-13)

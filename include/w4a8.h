@@ -146,6 +146,42 @@ w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, 
                                       int8_t* x_q, float* x_scale, hipStream_t stream);
 
 /*
+ * Streaming prefill attention with pre-RoPE cached keys.  FlashDrive, Sec.
+ * 3.1 ("Streaming design"): streaming inference encodes only the newest
+ * frame, inserts its tokens at the last-frame slot of each camera view
+ * (view-major layout) and keeps the KV cache of the earlier frames; keys are
+ * cached before their rotary embedding and rotated at their current,
+ * shifted window positions, and a streaming mask keeps cross-view causality
+ * with only the newest frame's tokens as queries.  This call computes, for
+ * every query head h and query i,
+ *     o[h][i] = sum_j softmax_j(scale * RoPE(q[h][i], pos_q[i]) . RoPE(k[h'][j], pos_k[j])) v[h'][j]
+ * over the keys j with pos_k[j] <= pos_q[i] (the causal order of the
+ * window), h' = h / (H / Hkv) (grouped-query heads).
+ *   RoPE: rotate-half pairs (d, d + 64) turned by the angles of the
+ *   caller's tables: y_d = x_d cos - x_{d+64} sin, y_{d+64} = x_{d+64} cos +
+ *   x_d sin, with cos = rope_cos[p][d], sin = rope_sin[p][d]; fp32 IEEE
+ *   operations, rounded to bf16.  Scores, softmax and the weighted sum run
+ *   in fp32 (bf16 MFMA operands: the rotated q and k, v and the softmax
+ *   weights); the output is rounded to bf16.
+ *   q            device, bf16 [H][Nq][D], 16-byte aligned
+ *   k, v         device, bf16 [Hkv][Nk][D] (the window's cache, any slot
+ *                order: positions carry the order), 16-byte aligned
+ *   pos_q, pos_k device, int32 [Nq], [Nk], window positions in [0, n_pos)
+ *                (positions outside are clamped for the table lookup)
+ *   rope_cos, rope_sin  device, fp32 [n_pos][D/2]
+ *   D            128 (W4A8_EUNSUPPORTED otherwise)
+ *   H, Hkv       1 <= Hkv, H % Hkv == 0
+ *   Nq, Nk       0 <= Nq (0 is a no-op), 1 <= Nk; both <= 2^24
+ *   scale        finite (e.g. 1/sqrt(D))
+ *   o            device, bf16 [H][Nq][D], 16-byte aligned
+ * A query that sees no key gets 0.  Does not synchronize.
+ */
+w4a8_status w4a8_stream_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v, const int32_t* pos_q,
+                                  const int32_t* pos_k, const float* rope_cos, const float* rope_sin, int64_t n_pos,
+                                  int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk, int64_t D, float scale, uint16_t* o,
+                                  hipStream_t stream);
+
+/*
  * Bytes of device workspace w4a8_linear needs for this problem (0 if none).
  * The workspace holds split-K partial sums and arrival counters (and, when
  * bf16 input is quantized by its own kernel, the int8 codes and scales).

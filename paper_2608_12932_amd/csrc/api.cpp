@@ -228,6 +228,39 @@ w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, 
                                                                                                   : W4A8_EHIP;
 }
 
+w4a8_status w4a8_stream_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v, const int32_t* pos_q,
+                                  const int32_t* pos_k, const float* rope_cos, const float* rope_sin, int64_t n_pos,
+                                  int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk, int64_t D, float scale, uint16_t* o,
+                                  hipStream_t stream) {
+  constexpr int64_t kMax = int64_t(1) << 24;
+  if (D != 128) return W4A8_EUNSUPPORTED;
+  if (H < 1 || Hkv < 1 || H % Hkv || H > 4096 || Nq < 0 || Nq > kMax || Nk < 1 || Nk > kMax || n_pos < 1 ||
+      n_pos > kMax)
+    return W4A8_EINVAL;
+  if (!(scale == scale) || scale > 3.4e38f || scale < -3.4e38f) return W4A8_EINVAL;  // finite
+  if (Nq == 0) return W4A8_OK;
+  if (!q || !k || !v || !pos_q || !pos_k || !rope_cos || !rope_sin || !o || !aligned(q, 16) || !aligned(k, 16) ||
+      !aligned(v, 16) || !aligned(o, 16) || !aligned(pos_q, 4) || !aligned(pos_k, 4) || !aligned(rope_cos, 4) ||
+      !aligned(rope_sin, 4))
+    return W4A8_EINVAL;
+  AttnArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.pos_q = pos_q;
+  a.pos_k = pos_k;
+  a.rope_cos = rope_cos;
+  a.rope_sin = rope_sin;
+  a.o = o;
+  a.H = (int)H;
+  a.Hkv = (int)Hkv;
+  a.Nq = (int)Nq;
+  a.Nk = (int)Nk;
+  a.n_pos = (int)n_pos;
+  a.scale_log2e = scale * 1.4426950408889634f;
+  return launch_stream_attention(a, stream) == hipSuccess ? W4A8_OK : W4A8_EHIP;
+}
+
 size_t w4a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind) {
   return workspace_bytes(M, N, K, scale_mode, in_kind, false);
 }

@@ -82,6 +82,21 @@ typedef void (*LargeMKernelFn)(const LargeMArgs);
 // for any tile but the gated one)
 LargeMKernelFn largem_group_kernel(int cfg, bool swiglu);
 
+// ---- streaming prefill attention (attention.hip)
+struct AttnArgs {
+  const uint16_t* q;      // bf16 [H][Nq][128], before the rotary embedding
+  const uint16_t* k;      // bf16 [Hkv][Nk][128], before the rotary embedding
+  const uint16_t* v;      // bf16 [Hkv][Nk][128]
+  const int32_t* pos_q;   // [Nq] window positions
+  const int32_t* pos_k;   // [Nk]
+  const float* rope_cos;  // [n_pos][64]
+  const float* rope_sin;  // [n_pos][64]
+  uint16_t* o;            // bf16 [H][Nq][128]
+  int H, Hkv, Nq, Nk, n_pos;
+  float scale_log2e;      // score scale times log2(e)
+};
+hipError_t launch_stream_attention(const AttnArgs& a, hipStream_t stream);
+
 const char* smallm_kernel_name(const SmallMPlan& p);
 const char* largem_kernel_name(const LargeMPlan& p);
 

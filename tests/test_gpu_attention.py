@@ -1,0 +1,98 @@
+"""Parity of the streaming prefill attention (w4a8_stream_attention) with
+the oracle (fp64 scores, softmax and sum over the same bf16-rounded rotated
+operands).
+
+Tolerance, derived: the kernel rounds the softmax weights to bf16 for the
+P V product (relative 2^-9 each, so at most 2^-9 sum_j P_ij |v_jd| per
+output), sums in fp32, and rounds the output to bf16 (2^-8 relative); its
+fp32 scores from exact bf16 products and its base-2 exponentials add
+errors far below those.  Written as |o - o64| <= 2^-8 |o64| + 2^-8 B with
+B = sum_j P_ij |v_jd| from the oracle (twice the weight term)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_12932_amd as w
+from paper_2608_12932_amd import inputs as I
+from helpers import dev
+
+pytestmark = pytest.mark.gpu
+
+D = 128
+
+
+def window(V, F, T, shift):
+    """A view-major window of V views x F frames x T tokens.  The cache
+    keeps each view's frames in a ring, slot (f + shift) % F holding frame f,
+    so slot order is not window order; the queries are the newest frame of
+    every view.  Returns (pos_k per cache slot, pos_q per query)."""
+    pos_k = np.empty(V * F * T, np.int32)
+    for v in range(V):
+        for f in range(F):
+            slot = (f + shift) % F
+            pos_k[(v * F + slot) * T:(v * F + slot + 1) * T] = v * F * T + f * T + np.arange(T)
+    pos_q = np.concatenate([v * F * T + (F - 1) * T + np.arange(T) for v in range(V)]).astype(np.int32)
+    return pos_k, pos_q
+
+
+def run(q, k, v, pos_q, pos_k, cos_t, sin_t, scale):
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev()).view(torch.bfloat16)
+    o = w.w4a8_stream_attention(t(q), t(k), t(v), torch.from_numpy(pos_q).to(dev()), torch.from_numpy(pos_k).to(dev()),
+                                torch.from_numpy(cos_t).to(dev()), torch.from_numpy(sin_t).to(dev()), scale)
+    torch.cuda.synchronize()
+    return (o.view(torch.int16).cpu().numpy().view(np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def check(H, Hkv, pos_q, pos_k, seed, label, rows=None):
+    Nq, Nk = len(pos_q), len(pos_k)
+    print(f"[case] stream attention {label} H={H} Hkv={Hkv} Nq={Nq} Nk={Nk}", flush=True)
+    q = I.activations(H * Nq, D, seed).reshape(H, Nq, D)
+    k = I.activations(Hkv * Nk, D, seed + 1).reshape(Hkv, Nk, D)
+    v = I.activations(Hkv * Nk, D, seed + 2).reshape(Hkv, Nk, D)
+    n_pos = int(max(pos_q.max(), pos_k.max())) + 1
+    cos_t, sin_t = oracle.rope_tables(n_pos, D, base=1e6)
+    scale = 1.0 / np.sqrt(D)
+    o = run(q, k, v, pos_q, pos_k, cos_t, sin_t, scale)
+    sel = np.arange(Nq) if rows is None else rows
+    o64, bnd = oracle.streaming_attention(q[:, sel], k, v, pos_q[sel], pos_k, cos_t, sin_t, np.float32(scale))
+    err = np.abs(o[:, sel] - o64)
+    bound = 2.0 ** -8 * np.abs(o64) + 2.0 ** -8 * bnd + 1e-30
+    bad = err > bound
+    assert not bad.any(), f"{label}: {bad.sum()} outputs outside tolerance, worst ratio {np.max(err / bound):.2f}"
+    return float(np.max(err / bound))
+
+
+@pytest.mark.parametrize("V,F,T,shift,H,Hkv", [(4, 4, 16, 0, 4, 2), (4, 4, 16, 3, 4, 4), (2, 3, 40, 1, 8, 2),
+                                               (4, 4, 23, 2, 2, 1)])
+def test_streaming_window(V, F, T, shift, H, Hkv):
+    # ragged query and key counts (not multiples of 64 and 32), ring-ordered slots
+    pos_k, pos_q = window(V, F, T, shift)
+    check(H, Hkv, pos_q, pos_k, 800 + T, f"window {V}x{F}x{T} shift {shift}")
+
+
+def test_streaming_window_realistic_size():
+    # 4 views x 4 frames x 192 tokens, 32 query heads on 8 kv heads (128 sampled queries)
+    pos_k, pos_q = window(4, 4, 192, 1)
+    rows = np.sort(np.random.Generator(np.random.PCG64(801)).choice(len(pos_q), 128, replace=False))
+    check(32, 8, pos_q, pos_k, 802, "4x4x192", rows=rows)
+
+
+def test_queries_seeing_one_key_and_all_keys():
+    # query positions below all but one key, and above every key
+    pos_k = np.arange(10, 110, dtype=np.int32)
+    pos_q = np.array([10, 11, 50, 109, 500, 10], np.int32)
+    check(2, 1, pos_q, pos_k, 803, "edge visibility")
+
+
+def test_rejected_calls():
+    L = w.lib()
+    import ctypes
+    P = ctypes.c_void_p
+    fake = P(1 << 20)
+    f = L.w4a8_stream_attention
+    args = lambda H=4, Hkv=2, Nq=8, Nk=16, Dd=128: (fake, fake, fake, fake, fake, fake, fake, 64, H, Hkv, Nq, Nk, Dd, 0.1, fake, None)
+    assert f(*args(Dd=64)) == w.W4A8_EUNSUPPORTED
+    assert f(*args(H=4, Hkv=3)) == w.W4A8_EINVAL
+    assert f(*args(Nk=0)) == w.W4A8_EINVAL
+    assert f(*args(Nq=0)) == w.W4A8_OK

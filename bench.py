@@ -42,6 +42,7 @@ sys.path.insert(0, ROOT)
 METRIC = "W4A8 linear: HBM GB/s at M=16, INT8 TOPS at M=1024 (% of roofline)"
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 INT8_PEAK_TOPS = 5000.0      # MI355X dense INT8 MFMA (5.0 POPS)
+BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA (2.5 PFLOP/s)
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["device.h", "kernels.h", "gemm_smallm.hip", "largem_kernel.h", "gemm_largem.hip",
                   "gemm_largem_group.hip", "quantize.hip", "api.cpp"]
@@ -382,6 +383,51 @@ def bench_rmsnorm_prologue(steps):
             "gemm": "gate+up N = 24576 on the int8 codes, per-channel scales", "rows": rows}
 
 
+def bench_stream_attention(steps):
+    """Streaming prefill attention of one layer: 4 views x 4 frames x 192
+    tokens in a ring-ordered view-major cache (3072 keys), the newest frame's
+    768 queries, 32 query heads on 8 kv heads, D = 128, graph-replayed.
+    Algorithmic flops count the visible (query, key) pairs only: 4 D per
+    pair (QK^T and PV); the kernel's work covers every pair."""
+    import torch
+    import paper_2608_12932_amd as w
+    from paper_2608_12932_amd import inputs as I
+
+    V, F, T, H, Hkv, D = 4, 4, 192, 32, 8, 128
+    pos_k = np.empty(V * F * T, np.int32)
+    for v in range(V):
+        for f in range(F):
+            slot = (f + 1) % F
+            pos_k[(v * F + slot) * T:(v * F + slot + 1) * T] = v * F * T + f * T + np.arange(T)
+    pos_q = np.concatenate([v * F * T + (F - 1) * T + np.arange(T) for v in range(V)]).astype(np.int32)
+    Nq, Nk = len(pos_q), len(pos_k)
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    q = t(I.activations(H * Nq, D, 90).reshape(H, Nq, D))
+    k = t(I.activations(Hkv * Nk, D, 91).reshape(Hkv, Nk, D))
+    v = t(I.activations(Hkv * Nk, D, 92).reshape(Hkv, Nk, D))
+    n_pos = V * F * T
+    ang = np.arange(n_pos, dtype=np.float64)[:, None] * 1e6 ** (-2.0 * np.arange(D // 2) / D)[None, :]
+    cos_t = torch.from_numpy(np.cos(ang).astype(np.float32)).to(dev)
+    sin_t = torch.from_numpy(np.sin(ang).astype(np.float32)).to(dev)
+    pq, pk = torch.from_numpy(pos_q).to(dev), torch.from_numpy(pos_k).to(dev)
+    o = torch.empty((H, Nq, D), dtype=torch.bfloat16, device=dev)
+    L = w.lib()
+    ptrs = (q.data_ptr(), k.data_ptr(), v.data_ptr(), pq.data_ptr(), pk.data_ptr(), cos_t.data_ptr(), sin_t.data_ptr())
+
+    def call(i, stream):
+        L.w4a8_stream_attention(*ptrs, n_pos, H, Hkv, Nq, Nk, D, 1.0 / np.sqrt(D), o.data_ptr(), stream)
+
+    ms = graph_ms(call, steps)
+    visible = int((pos_k[None, :] <= pos_q[:, None]).sum())
+    flops = 4 * H * D * visible
+    tflops = flops / (ms * 1e-3) / 1e12
+    return {"workload": f"streaming prefill attention, {V} views x {F} frames x {T} tokens, H={H}, Hkv={Hkv}, D={D}",
+            "Nq": Nq, "Nk": Nk, "us": round(ms * 1e3, 3), "visible_pairs": visible,
+            "algorithmic_flops": flops, "TFLOP/s": round(tflops, 1), "peak": BF16_PEAK_TFLOPS,
+            "frac_bf16": round(tflops / BF16_PEAK_TFLOPS, 4)}
+
+
 def bench_layer_group(steps, warmup, copies=6):
     """One decoder layer's four linears (QKV, O, gate+up, down) with group-128
     fp16 scales; a step is the four calls, each on its own bf16 x.  Six copies
@@ -564,6 +610,7 @@ def main():
         print(json.dumps({"sweep": {"down_verify": bench_down_verify(ss, sw),
                                     "gate_up_swiglu": bench_gate_up_swiglu(ss, sw),
                                     "rmsnorm_prologue": bench_rmsnorm_prologue(ss),
+                                    "stream_attention": bench_stream_attention(ss),
                                     "layer_group": bench_layer_group(ss, sw),
                                     "stack": bench_stack(max(10, args.steps // 50))}}), flush=True)
         return
@@ -618,6 +665,7 @@ def main():
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
         out["sweep"] = {"down_verify": bench_down_verify(ss, sw), "gate_up_swiglu": bench_gate_up_swiglu(ss, sw),
                         "rmsnorm_prologue": bench_rmsnorm_prologue(ss),
+                        "stream_attention": bench_stream_attention(ss),
                         "layer_group": bench_layer_group(ss, sw),
                         "stack": bench_stack(max(10, args.steps // 50))}
     if not args.no_cpu_baseline:

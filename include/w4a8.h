@@ -168,18 +168,27 @@ w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, 
  *                order: positions carry the order), 16-byte aligned
  *   pos_q, pos_k device, int32 [Nq], [Nk], window positions in [0, n_pos)
  *                (positions outside are clamped for the table lookup)
- *   rope_cos, rope_sin  device, fp32 [n_pos][D/2]
+ *   rope_cos, rope_sin  device, fp32 [n_pos][D/2], 16-byte aligned
  *   D            128 (W4A8_EUNSUPPORTED otherwise)
  *   H, Hkv       1 <= Hkv, H % Hkv == 0
- *   Nq, Nk       0 <= Nq (0 is a no-op), 1 <= Nk; both <= 2^24
+ *   Nq, Nk       0 <= Nq (0 is a no-op), 1 <= Nk; both <= 2^22
  *   scale        finite (e.g. 1/sqrt(D))
  *   o            device, bf16 [H][Nq][D], 16-byte aligned
- * A query that sees no key gets 0.  Does not synchronize.
+ *   workspace    device, >= w4a8_stream_attention_workspace_bytes(H, Nq, Nk)
+ *                bytes, 256-byte aligned (may be NULL if that is 0): the
+ *                partial results of key-range splits, written before read
+ *                (no zero fill needed); concurrent calls must not share it
+ * A query that sees no key gets 0.  Does not synchronize; enqueues kernels
+ * only.
  */
 w4a8_status w4a8_stream_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v, const int32_t* pos_q,
                                   const int32_t* pos_k, const float* rope_cos, const float* rope_sin, int64_t n_pos,
                                   int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk, int64_t D, float scale, uint16_t* o,
-                                  hipStream_t stream);
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes w4a8_stream_attention needs (0 if none, and 0 for shapes
+ * it rejects). */
+size_t w4a8_stream_attention_workspace_bytes(int64_t H, int64_t Nq, int64_t Nk);
 
 /*
  * Bytes of device workspace w4a8_linear needs for this problem (0 if none).

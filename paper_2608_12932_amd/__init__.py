@@ -26,7 +26,8 @@ GROUP_SIZE = 128
 EXPORTS = ("w4a8_status_string", "w4a8_packed_weight_bytes", "w4a8_pack_weights",
            "w4a8_quantize_act", "w4a8_linear_workspace_bytes", "w4a8_linear",
            "w4a8_linear_describe", "w4a8_linear_swiglu", "w4a8_linear_swiglu_workspace_bytes",
-           "w4a8_linear_swiglu_describe", "w4a8_rmsnorm_quantize_act", "w4a8_stream_attention")
+           "w4a8_linear_swiglu_describe", "w4a8_rmsnorm_quantize_act", "w4a8_stream_attention",
+           "w4a8_stream_attention_workspace_bytes")
 
 _OUT_DTYPE = {OUT_BF16: torch.bfloat16, OUT_F32: torch.float32, OUT_I32_ACC: torch.int32}
 
@@ -59,8 +60,11 @@ def lib() -> ctypes.CDLL:
         L.w4a8_quantize_act.restype = I
         L.w4a8_rmsnorm_quantize_act.argtypes = [P, P, ctypes.c_float, I64, I64, P, P, P]
         L.w4a8_rmsnorm_quantize_act.restype = I
-        L.w4a8_stream_attention.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, ctypes.c_float, P, P]
+        L.w4a8_stream_attention.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, ctypes.c_float, P,
+                                            P, SZ, P]
         L.w4a8_stream_attention.restype = I
+        L.w4a8_stream_attention_workspace_bytes.argtypes = [I64, I64, I64]
+        L.w4a8_stream_attention_workspace_bytes.restype = SZ
         L.w4a8_linear_workspace_bytes.argtypes = [I64, I64, I64, I, I]
         L.w4a8_linear_workspace_bytes.restype = SZ
         L.w4a8_linear.argtypes = [P, I, P, I64, I64, P, P, I, I64, P, I, P, SZ, P]
@@ -249,7 +253,8 @@ def w4a8_linear_swiglu(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.T
 
 def w4a8_stream_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos_q: torch.Tensor,
                           pos_k: torch.Tensor, rope_cos: torch.Tensor, rope_sin: torch.Tensor, scale: float,
-                          out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+                          out: torch.Tensor | None = None, workspace: Workspace | torch.Tensor | None = None,
+                          stream=None) -> torch.Tensor:
     """Streaming prefill attention: q bf16 [H][Nq][128] and the pre-RoPE
     cache k, v bf16 [Hkv][Nk][128], int32 window positions pos_q [Nq] and
     pos_k [Nk], fp32 rotary tables [n_pos][64] -> bf16 [H][Nq][128]; key j is
@@ -266,10 +271,22 @@ def w4a8_stream_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos
         out = torch.empty((H, Nq, D), dtype=torch.bfloat16, device=q.device)
     elif tuple(out.shape) != (H, Nq, D):
         raise ValueError(f"out must be [{H}][{Nq}][{D}]")
+    need = int(lib().w4a8_stream_attention_workspace_bytes(H, Nq, Nk)) if Nq else 0
+    if need == 0:
+        wk_ptr, wk_bytes = None, 0
+    else:
+        if workspace is None:
+            workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        buf = workspace.get(need) if isinstance(workspace, Workspace) else workspace
+        wk_ptr, wk_bytes = _dev(buf, "workspace", torch.uint8), buf.numel()
     rc = lib().w4a8_stream_attention(_dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
                                      _dev(v, "v", torch.bfloat16), _dev(pos_q, "pos_q", torch.int32),
                                      _dev(pos_k, "pos_k", torch.int32), _dev(rope_cos, "rope_cos", torch.float32),
                                      _dev(rope_sin, "rope_sin", torch.float32), rope_cos.shape[0], H, Hkv, Nq, Nk, D,
-                                     float(scale), _dev(out, "out", torch.bfloat16), _stream(stream))
+                                     float(scale), _dev(out, "out", torch.bfloat16), wk_ptr, wk_bytes, _stream(stream))
     _check(rc, "w4a8_stream_attention")
     return out
+
+
+def w4a8_stream_attention_workspace_bytes(H: int, Nq: int, Nk: int) -> int:
+    return int(lib().w4a8_stream_attention_workspace_bytes(H, Nq, Nk))

@@ -228,11 +228,17 @@ w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, 
                                                                                                   : W4A8_EHIP;
 }
 
+size_t w4a8_stream_attention_workspace_bytes(int64_t H, int64_t Nq, int64_t Nk) {
+  constexpr int64_t kMax = int64_t(1) << 22;
+  if (H < 1 || H > 4096 || Nq < 1 || Nq > kMax || Nk < 1 || Nk > kMax) return 0;
+  return stream_attention_workspace((int)H, (int)Nq, (int)Nk);
+}
+
 w4a8_status w4a8_stream_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v, const int32_t* pos_q,
                                   const int32_t* pos_k, const float* rope_cos, const float* rope_sin, int64_t n_pos,
                                   int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk, int64_t D, float scale, uint16_t* o,
-                                  hipStream_t stream) {
-  constexpr int64_t kMax = int64_t(1) << 24;
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  constexpr int64_t kMax = int64_t(1) << 22;  // 32-bit buffer offsets over a head's [N][128] rows
   if (D != 128) return W4A8_EUNSUPPORTED;
   if (H < 1 || Hkv < 1 || H % Hkv || H > 4096 || Nq < 0 || Nq > kMax || Nk < 1 || Nk > kMax || n_pos < 1 ||
       n_pos > kMax)
@@ -240,10 +246,13 @@ w4a8_status w4a8_stream_attention(const uint16_t* q, const uint16_t* k, const ui
   if (!(scale == scale) || scale > 3.4e38f || scale < -3.4e38f) return W4A8_EINVAL;  // finite
   if (Nq == 0) return W4A8_OK;
   if (!q || !k || !v || !pos_q || !pos_k || !rope_cos || !rope_sin || !o || !aligned(q, 16) || !aligned(k, 16) ||
-      !aligned(v, 16) || !aligned(o, 16) || !aligned(pos_q, 4) || !aligned(pos_k, 4) || !aligned(rope_cos, 4) ||
-      !aligned(rope_sin, 4))
+      !aligned(v, 16) || !aligned(o, 16) || !aligned(pos_q, 4) || !aligned(pos_k, 4) || !aligned(rope_cos, 16) ||
+      !aligned(rope_sin, 16))
     return W4A8_EINVAL;
+  const size_t need = stream_attention_workspace((int)H, (int)Nq, (int)Nk);
+  if (workspace_bytes < need || (need && (!workspace || !aligned(workspace, 256)))) return W4A8_EINVAL;
   AttnArgs a{};
+  a.workspace = workspace;
   a.q = q;
   a.k = k;
   a.v = v;

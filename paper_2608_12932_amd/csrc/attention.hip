@@ -9,7 +9,8 @@
 // view-major window.
 //
 // One workgroup per (64 queries, head); each of its 4 waves owns 16
-// queries.  Per 32-key tile:
+// queries.  Key tiles that none of its queries can see are skipped.  Per
+// 32-key tile:
 //   - the workgroup stages the rotated keys (bf16, [key][d]) and the values
 //     transposed ([d][key]) in LDS;
 //   - a wave forms S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (its rotated
@@ -39,7 +40,11 @@ constexpr int kQPerWave = 16;
 constexpr int kAttnWaves = 4;
 constexpr int kQPerBlock = kQPerWave * kAttnWaves;
 constexpr int kKeys = 32;        // keys per tile
-constexpr int kVtPitch = kKeys + 8;  // bf16 elements per row of the transposed value tile
+// LDS row pitches (bf16 elements), padded against bank conflicts: the key
+// rows' 16-byte reads by 16 lanes (one per key) and the transposed value
+// tile's dword writes (two keys of one d) and 8-byte reads
+constexpr int kKPitch = kD + 8;
+constexpr int kVtPitch = kKeys + 4;
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8_t, u); }
 
@@ -61,14 +66,23 @@ __device__ __forceinline__ void rotate_chunks(uint4 a8, uint4 b8, const float* c
   hi = make_uint4(hw[0], hw[1], hw[2], hw[3]);
 }
 
+// Per-tile minimum key positions kept for the skip test (tiles beyond this
+// count are never skipped).
+constexpr int kMaxSkipTiles = 2048;
+
 __global__ __launch_bounds__(kAttnWaves * 64) void stream_attention(const AttnArgs a) {
-  __shared__ __align__(16) uint16_t l_k[kKeys * kD];          // rotated keys [key][d]
-  __shared__ __align__(16) uint16_t l_vt[kD * kVtPitch];      // values transposed [d][key]
-  __shared__ int l_pos[kKeys];
+  // two stages of the key / value tile: the next visible tile is staged
+  // while the current one is computed
+  __shared__ __align__(16) uint16_t l_k[2][kKeys * kKPitch];     // rotated keys [key][d]
+  __shared__ __align__(16) uint16_t l_vt[2][kD * kVtPitch];      // values transposed [d][key]
+  __shared__ int l_pos[2][kKeys];
+  __shared__ int l_tmin[kMaxSkipTiles];
+  __shared__ int l_qmax[kAttnWaves];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = blockIdx.y, hk = h / (a.H / a.Hkv);
+  const int split = blockIdx.z;
   const int r16 = lane & 15, g = lane >> 4;
   const int P = a.n_pos;
   auto clamp_pos = [&](int p) { return p < 0 ? 0 : (p >= P ? P - 1 : p); };  // table reads stay in bounds
@@ -79,15 +93,19 @@ __global__ __launch_bounds__(kAttnWaves * 64) void stream_attention(const AttnAr
   const int qi = blockIdx.x * kQPerBlock + wave * kQPerWave + r16;
   const bool q_ok = qi < a.Nq;
   const int pq = q_ok ? a.pos_q[qi] : INT_MIN;
+  // Rows past Nq and keys past Nk are out-of-range buffer offsets, which
+  // read zeros (selects of a loaded value against a zero vector had put the
+  // zero in scratch memory, on the loop's critical path).
+  const __amdgpu_buffer_rsrc_t qres = make_rsrc(a.q + (size_t)h * a.Nq * kD, (uint32_t)((size_t)a.Nq * kD * 2));
   bf16x8_t qf[4];
   {
-    const uint4* qrow = reinterpret_cast<const uint4*>(a.q + ((size_t)h * a.Nq + (q_ok ? qi : 0)) * kD);
+    const uint32_t qoff = q_ok ? (uint32_t)(qi * kD * 2) : kOOB;
     const int pc = clamp_pos(q_ok ? pq : 0);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int d = 32 * i + 8 * g;  // < 64
-      uint4 x0 = q_ok ? qrow[d / 8] : make_uint4(0, 0, 0, 0);
-      uint4 x1 = q_ok ? qrow[(d + kHalf) / 8] : make_uint4(0, 0, 0, 0);
+      const uint4 x0 = buf_load16(qres, qoff == kOOB ? kOOB : qoff + d * 2);
+      const uint4 x1 = buf_load16(qres, qoff == kOOB ? kOOB : qoff + (d + kHalf) * 2);
       uint4 lo, hi;
       rotate_chunks(x0, x1, a.rope_cos + (size_t)pc * kHalf + d, a.rope_sin + (size_t)pc * kHalf + d, lo, hi);
       qf[i] = as_bf16x8(lo);
@@ -95,44 +113,91 @@ __global__ __launch_bounds__(kAttnWaves * 64) void stream_attention(const AttnAr
     }
   }
 
+  // ---- this workgroup's key tiles (its split of the key range) and the
+  // skip test: a tile none of its queries can see (every key position above
+  // the largest query position) is not staged
+  const int ntiles_all = (a.Nk + kKeys - 1) / kKeys;
+  const int t_begin = split * a.tiles_per_split;
+  const int ntiles = min(ntiles_all, t_begin + a.tiles_per_split);  // one past the last tile
+  const bool skipping = ntiles - t_begin <= kMaxSkipTiles;
+  {
+    int qm = pq;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) qm = max(qm, __shfl_xor(qm, off, 64));
+    if (lane == 0) l_qmax[wave] = qm;
+    // 32 threads per tile (one key each), 8 tiles per pass
+    if (skipping)
+      for (int t0 = t_begin; t0 < ntiles; t0 += kAttnWaves * 64 / kKeys) {
+        const int t = t0 + tid / kKeys, j = t * kKeys + tid % kKeys;
+        int mn = t < ntiles && j < a.Nk ? a.pos_k[j] : INT_MAX;
+#pragma unroll
+        for (int off = kKeys / 2; off >= 1; off >>= 1) mn = min(mn, __shfl_xor(mn, off, 64));
+        if (tid % kKeys == 0 && t < ntiles) l_tmin[t - t_begin] = mn;
+      }
+  }
+  __syncthreads();
+  int wg_qmax = l_qmax[0];
+#pragma unroll
+  for (int w = 1; w < kAttnWaves; ++w) wg_qmax = max(wg_qmax, l_qmax[w]);
+  auto next_visible = [&](int t) {
+    if (skipping)
+      while (t < ntiles && l_tmin[t - t_begin] > wg_qmax) ++t;
+    return t;
+  };
+
   f32x4_t acc[kD / 16];
 #pragma unroll
   for (int t = 0; t < kD / 16; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, lsum = 0.0f;
   const float sl2 = a.scale_log2e;
 
-  const uint16_t* kbase = a.k + (size_t)hk * a.Nk * kD;
-  const uint16_t* vbase = a.v + (size_t)hk * a.Nk * kD;
-  // staging: thread tid handles key tid / 8 of the tile and the pair of
-  // 8-element chunks (8 c, 64 + 8 c), c = tid % 8
+  const __amdgpu_buffer_rsrc_t kres = make_rsrc(a.k + (size_t)hk * a.Nk * kD, (uint32_t)((size_t)a.Nk * kD * 2));
+  const __amdgpu_buffer_rsrc_t vres = make_rsrc(a.v + (size_t)hk * a.Nk * kD, (uint32_t)((size_t)a.Nk * kD * 2));
+  // staging: for the keys, thread tid handles key tid / 8 of the tile and
+  // the pair of 8-element chunks (8 c, 64 + 8 c), c = tid % 8; for the
+  // values, keys 2 kp and 2 kp + 1 (kp = tid % 16) and d chunk tid / 16, so
+  // that each transposed store is one dword.  The global loads of the next
+  // tile are issued before the current tile's compute.
   const int sj = tid >> 3, sc = tid & 7;
-  for (int k0 = 0; k0 < a.Nk; k0 += kKeys) {
-    {
-      const int j = k0 + sj;
-      const bool ok = j < a.Nk;
-      const uint4* krow = reinterpret_cast<const uint4*>(kbase + (size_t)(ok ? j : 0) * kD);
-      const uint4* vrow = reinterpret_cast<const uint4*>(vbase + (size_t)(ok ? j : 0) * kD);
-      const int pj = ok ? a.pos_k[j] : INT_MAX;
-      const int pc = clamp_pos(ok ? pj : 0);
-      const uint4 z = make_uint4(0, 0, 0, 0);
-      uint4 lo, hi;
-      rotate_chunks(ok ? krow[sc] : z, ok ? krow[sc + 8] : z, a.rope_cos + (size_t)pc * kHalf + 8 * sc,
-                    a.rope_sin + (size_t)pc * kHalf + 8 * sc, lo, hi);
-      *reinterpret_cast<uint4*>(&l_k[sj * kD + 8 * sc]) = lo;
-      *reinterpret_cast<uint4*>(&l_k[sj * kD + kHalf + 8 * sc]) = hi;
-      const uint4 v0 = ok ? vrow[sc] : z, v1 = ok ? vrow[sc + 8] : z;
-      const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w}, w1[4] = {v1.x, v1.y, v1.z, v1.w};
+  const int vkp = tid & 15, vc = tid >> 4;
+  uint4 gk0, gk1, gv0, gv1;
+  float gcs[8], gsn[8];
+  int gpj;
+  auto load_tile = [&](int t) {
+    const int j = t * kKeys + sj;
+    const bool ok = j < a.Nk;
+    const int jv0 = t * kKeys + 2 * vkp, jv1 = jv0 + 1;
+    gpj = ok ? a.pos_k[j] : INT_MAX;
+    const uint32_t ko = ok ? (uint32_t)((j * kD + 8 * sc) * 2) : kOOB;
+    gk0 = buf_load16(kres, ko);
+    gk1 = buf_load16(kres, ko == kOOB ? kOOB : ko + kHalf * 2);
+    gv0 = buf_load16(vres, jv0 < a.Nk ? (uint32_t)((jv0 * kD + 8 * vc) * 2) : kOOB);
+    gv1 = buf_load16(vres, jv1 < a.Nk ? (uint32_t)((jv1 * kD + 8 * vc) * 2) : kOOB);
+    const int pc = clamp_pos(ok ? gpj : 0);
+    const float4* cp = reinterpret_cast<const float4*>(a.rope_cos + (size_t)pc * kHalf + 8 * sc);
+    const float4* sp = reinterpret_cast<const float4*>(a.rope_sin + (size_t)pc * kHalf + 8 * sc);
+    const float4 c0 = cp[0], c1 = cp[1], s0 = sp[0], s1 = sp[1];
+    gcs[0] = c0.x; gcs[1] = c0.y; gcs[2] = c0.z; gcs[3] = c0.w; gcs[4] = c1.x; gcs[5] = c1.y; gcs[6] = c1.z; gcs[7] = c1.w;
+    gsn[0] = s0.x; gsn[1] = s0.y; gsn[2] = s0.z; gsn[3] = s0.w; gsn[4] = s1.x; gsn[5] = s1.y; gsn[6] = s1.z; gsn[7] = s1.w;
+  };
+  auto store_tile = [&](int b) {
+    uint4 lo, hi;
+    rotate_chunks(gk0, gk1, gcs, gsn, lo, hi);
+    *reinterpret_cast<uint4*>(&l_k[b][sj * kKPitch + 8 * sc]) = lo;
+    *reinterpret_cast<uint4*>(&l_k[b][sj * kKPitch + kHalf + 8 * sc]) = hi;
+    // row d of the transposed tile gets (v[2 kp][d], v[2 kp + 1][d]) as one dword
+    const uint32_t w0[4] = {gv0.x, gv0.y, gv0.z, gv0.w}, w1[4] = {gv1.x, gv1.y, gv1.z, gv1.w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        l_vt[(8 * sc + 2 * e) * kVtPitch + sj] = (uint16_t)(w0[e] & 0xFFFFu);
-        l_vt[(8 * sc + 2 * e + 1) * kVtPitch + sj] = (uint16_t)(w0[e] >> 16);
-        l_vt[(kHalf + 8 * sc + 2 * e) * kVtPitch + sj] = (uint16_t)(w1[e] & 0xFFFFu);
-        l_vt[(kHalf + 8 * sc + 2 * e + 1) * kVtPitch + sj] = (uint16_t)(w1[e] >> 16);
-      }
-      if (sc == 0) l_pos[sj] = pj;
+    for (int e = 0; e < 4; ++e) {
+      uint32_t* r0 = reinterpret_cast<uint32_t*>(&l_vt[b][(8 * vc + 2 * e) * kVtPitch + 2 * vkp]);
+      uint32_t* r1 = reinterpret_cast<uint32_t*>(&l_vt[b][(8 * vc + 2 * e + 1) * kVtPitch + 2 * vkp]);
+      *r0 = __builtin_amdgcn_perm(w1[e], w0[e], 0x05040100u);  // low halves: d = 8 vc + 2 e
+      *r1 = __builtin_amdgcn_perm(w1[e], w0[e], 0x07060302u);  // high halves: d + 1
     }
-    __syncthreads();
+    if (sc == 0) l_pos[b][sj] = gpj;
+  };
 
+  auto compute_tile = [&](int b) {
     // ---- S^T for keys 16 u + (4 g + r), u = 0, 1: lane holds query r16
     float s[2][4];
 #pragma unroll
@@ -140,12 +205,12 @@ __global__ __launch_bounds__(kAttnWaves * 64) void stream_attention(const AttnAr
       f32x4_t c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const bf16x8_t kf = as_bf16x8(*reinterpret_cast<const uint4*>(&l_k[(16 * u + r16) * kD + 32 * i + 8 * g]));
+        const bf16x8_t kf = as_bf16x8(*reinterpret_cast<const uint4*>(&l_k[b][(16 * u + r16) * kKPitch + 32 * i + 8 * g]));
         c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[i], c, 0, 0, 0);
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const bool vis = l_pos[16 * u + 4 * g + r] <= pq;
+        const bool vis = l_pos[b][16 * u + 4 * g + r] <= pq;
         s[u][r] = vis ? c[r] * sl2 : -INFINITY;
       }
     }
@@ -178,7 +243,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void stream_attention(const AttnAr
     // ---- O^T += V^T P^T: A row d = 16 t + r16, the same 8 keys
 #pragma unroll
     for (int t = 0; t < kD / 16; ++t) {
-      const uint16_t* vr = &l_vt[(16 * t + r16) * kVtPitch];
+      const uint16_t* vr = &l_vt[b][(16 * t + r16) * kVtPitch];
       const uint2 va = *reinterpret_cast<const uint2*>(vr + 4 * g);
       const uint2 vb = *reinterpret_cast<const uint2*>(vr + 16 + 4 * g);
       const bf16x8_t vf = as_bf16x8(make_uint4(va.x, va.y, vb.x, vb.y));
@@ -186,13 +251,42 @@ __global__ __launch_bounds__(kAttnWaves * 64) void stream_attention(const AttnAr
       for (int r = 0; r < 4; ++r) acc[t][r] *= alpha;
       acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, acc[t], 0, 0, 0);
     }
-    __syncthreads();  // the next tile overwrites the staged keys and values
+  };
+
+  // One barrier per tile: stage b is computed while stage b ^ 1 is filled;
+  // stage b ^ 1 was last read before the previous barrier.
+  int cur = next_visible(t_begin);
+  if (cur < ntiles) {
+    load_tile(cur);
+    store_tile(0);
+  }
+  __syncthreads();
+  int b = 0;
+  while (cur < ntiles) {
+    const int nxt = next_visible(cur + 1);
+    if (nxt < ntiles) load_tile(nxt);
+    compute_tile(b);
+    if (nxt < ntiles) store_tile(b ^ 1);
+    __syncthreads();
+    b ^= 1;
+    cur = nxt;
   }
 
   // ---- O = O^T / l: lane holds query r16, d = 16 t + 4 g + r
   lsum += __shfl_xor(lsum, 16, 64);
   lsum += __shfl_xor(lsum, 32, 64);
   if (!q_ok) return;
+  if (a.S > 1) {
+    // a split's partial result: the unnormalized sum, its running maximum
+    // (base 2, scaled scores) and weight total; attn_combine merges them
+    const size_t row = ((size_t)split * a.H + h) * a.Nq + qi;
+    float* po = a.part_o + row * kD;
+#pragma unroll
+    for (int t = 0; t < kD / 16; ++t)
+      *reinterpret_cast<float4*>(po + 16 * t + 4 * g) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+    if (g == 0) *reinterpret_cast<float2*>(a.part_ml + row * 2) = make_float2(m, lsum);
+    return;
+  }
   const float inv = lsum > 0.0f ? __fdiv_rn(1.0f, lsum) : 0.0f;  // a query that sees no key gets 0
   uint16_t* orow = a.o + ((size_t)h * a.Nq + qi) * kD;
 #pragma unroll
@@ -202,12 +296,71 @@ __global__ __launch_bounds__(kAttnWaves * 64) void stream_attention(const AttnAr
   }
 }
 
+
+// Merge of the splits' partial results: thread per (head, query, 8 of d).
+__global__ __launch_bounds__(256) void attn_combine(const AttnArgs a) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t rows = (size_t)a.H * a.Nq;
+  if (idx >= rows * (kD / 8)) return;
+  const size_t row = idx / (kD / 8);
+  const int c = (int)(idx % (kD / 8));
+  float mmax = -INFINITY;
+  for (int s = 0; s < a.S; ++s) mmax = fmaxf(mmax, a.part_ml[((size_t)s * rows + row) * 2]);
+  float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, l = 0.0f;
+  if (mmax != -INFINITY) {
+    for (int s = 0; s < a.S; ++s) {
+      const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + ((size_t)s * rows + row) * 2);
+      if (ml.x == -INFINITY) continue;  // the split saw no key of this query
+      const float wgt = exp2f(ml.x - mmax);
+      l += ml.y * wgt;
+      const float4* po = reinterpret_cast<const float4*>(a.part_o + ((size_t)s * rows + row) * kD + 8 * c);
+      const float4 u0 = po[0], u1 = po[1];
+      o[0] += u0.x * wgt; o[1] += u0.y * wgt; o[2] += u0.z * wgt; o[3] += u0.w * wgt;
+      o[4] += u1.x * wgt; o[5] += u1.y * wgt; o[6] += u1.z * wgt; o[7] += u1.w * wgt;
+    }
+  }
+  const float inv = l > 0.0f ? __fdiv_rn(1.0f, l) : 0.0f;
+  *reinterpret_cast<uint4*>(a.o + row * kD + 8 * c) =
+      make_uint4(bf16x2_bits(o[0] * inv, o[1] * inv), bf16x2_bits(o[2] * inv, o[3] * inv),
+                 bf16x2_bits(o[4] * inv, o[5] * inv), bf16x2_bits(o[6] * inv, o[7] * inv));
+}
+
 }  // namespace
 
-hipError_t launch_stream_attention(const AttnArgs& a, hipStream_t stream) {
-  if (a.Nq == 0) return hipSuccess;
-  const dim3 grid((unsigned)((a.Nq + kQPerBlock - 1) / kQPerBlock), (unsigned)a.H);
+// Key-range splits: enough workgroups to fill the chip about four times over
+// (at most 8 splits, at least 8 tiles each); the heaviest workgroups, whose
+// queries see the whole window, otherwise run every tile in series.
+int stream_attention_splits(int H, int Nq, int Nk) {
+  const long blocks = (long)((Nq + kQPerBlock - 1) / kQPerBlock) * H;
+  const int ntiles = (Nk + kKeys - 1) / kKeys;
+  int S = 1;
+  while (S < 8 && blocks * S * 2 <= 2048 && ntiles / (S * 2) >= 8) S *= 2;
+  return S;
+}
+
+size_t stream_attention_workspace(int H, int Nq, int Nk) {
+  const int S = stream_attention_splits(H, Nq, Nk);
+  if (S == 1) return 0;
+  return (size_t)S * H * Nq * (kD + 2) * sizeof(float);
+}
+
+hipError_t launch_stream_attention(const AttnArgs& a0, hipStream_t stream) {
+  if (a0.Nq == 0) return hipSuccess;
+  AttnArgs a = a0;
+  const int ntiles = (a.Nk + kKeys - 1) / kKeys;
+  a.S = stream_attention_splits(a.H, a.Nq, a.Nk);
+  a.tiles_per_split = (ntiles + a.S - 1) / a.S;
+  a.S = (ntiles + a.tiles_per_split - 1) / a.tiles_per_split;  // no empty trailing split
+  if (a.S > 1) {
+    a.part_o = static_cast<float*>(a.workspace);
+    a.part_ml = a.part_o + (size_t)a.S * a.H * a.Nq * kD;
+  }
+  const dim3 grid((unsigned)((a.Nq + kQPerBlock - 1) / kQPerBlock), (unsigned)a.H, (unsigned)a.S);
   stream_attention<<<grid, dim3(kAttnWaves * 64), 0, stream>>>(a);
+  if (a.S > 1) {
+    const size_t threads = (size_t)a.H * a.Nq * (kD / 8);
+    attn_combine<<<dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream>>>(a);
+  }
   return hipGetLastError();
 }
 

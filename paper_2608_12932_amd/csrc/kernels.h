@@ -94,8 +94,15 @@ struct AttnArgs {
   uint16_t* o;            // bf16 [H][Nq][128]
   int H, Hkv, Nq, Nk, n_pos;
   float scale_log2e;      // score scale times log2(e)
+  void* workspace;        // split partial results (stream_attention_workspace bytes)
+  // set by the launcher
+  int S, tiles_per_split;
+  float* part_o;          // [S][H][Nq][128] unnormalized partial sums
+  float* part_ml;         // [S][H][Nq][2] running maximum (base 2) and weight total
 };
 hipError_t launch_stream_attention(const AttnArgs& a, hipStream_t stream);
+int stream_attention_splits(int H, int Nq, int Nk);
+size_t stream_attention_workspace(int H, int Nq, int Nk);
 
 const char* smallm_kernel_name(const SmallMPlan& p);
 const char* largem_kernel_name(const LargeMPlan& p);

@@ -78,6 +78,15 @@ def test_streaming_window_realistic_size():
     check(32, 8, pos_q, pos_k, 802, "4x4x192", rows=rows)
 
 
+def test_key_range_splits():
+    # few query blocks over a long cache: the key range is split over
+    # workgroups and merged (8 splits here; early queries see no key of the
+    # later splits), with a ragged last tile
+    pos_k, pos_q = window(4, 4, 125, 2)
+    assert w.w4a8_stream_attention_workspace_bytes(2, len(pos_q), len(pos_k)) > 0
+    check(2, 1, pos_q, pos_k, 804, "splits 4x4x125")
+
+
 def test_queries_seeing_one_key_and_all_keys():
     # query positions below all but one key, and above every key
     pos_k = np.arange(10, 110, dtype=np.int32)
@@ -91,8 +100,12 @@ def test_rejected_calls():
     P = ctypes.c_void_p
     fake = P(1 << 20)
     f = L.w4a8_stream_attention
-    args = lambda H=4, Hkv=2, Nq=8, Nk=16, Dd=128: (fake, fake, fake, fake, fake, fake, fake, 64, H, Hkv, Nq, Nk, Dd, 0.1, fake, None)
+    args = lambda H=4, Hkv=2, Nq=8, Nk=16, Dd=128: (fake, fake, fake, fake, fake, fake, fake, 64, H, Hkv, Nq, Nk, Dd,
+                                                    0.1, fake, None, 0, None)
     assert f(*args(Dd=64)) == w.W4A8_EUNSUPPORTED
     assert f(*args(H=4, Hkv=3)) == w.W4A8_EINVAL
     assert f(*args(Nk=0)) == w.W4A8_EINVAL
     assert f(*args(Nq=0)) == w.W4A8_OK
+    # a split shape without its workspace
+    assert w.w4a8_stream_attention_workspace_bytes(32, 768, 3072) > 0
+    assert f(*args(H=32, Hkv=8, Nq=768, Nk=3072)) == w.W4A8_EINVAL

@@ -68,7 +68,7 @@ __device__ __forceinline__ void rotate_chunks(uint4 a8, uint4 b8, const float* c
 
 // Per-tile minimum key positions kept for the skip test (tiles beyond this
 // count are never skipped).
-constexpr int kMaxSkipTiles = 2048;
+constexpr int kMaxSkipTiles = 512;
 
 __global__ __launch_bounds__(kAttnWaves * 64) void stream_attention(const AttnArgs a) {
   // two stages of the key / value tile: the next visible tile is staged

@@ -56,6 +56,12 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def file_hash(name: str) -> str:
+    """Short hash of one kernel source file."""
+    with open(os.path.join(ROOT, "paper_2608_12932_amd", "csrc", name), "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
 def counter_traffic(name: str):
     """HBM bytes per dispatch from a committed rocprofv3 counter summary, or
     None if there is none or the kernels changed since it was taken."""
@@ -600,10 +606,12 @@ def main():
                     help="skip the down-projection verify and group-scale layer sweeps")
     ap.add_argument("--sweep-only", action="store_true",
                     help="run only the sweeps (for profiling their kernels); prints the sweep object")
+    ap.add_argument("--attention-only", action="store_true",
+                    help="run only the streaming attention workload (for profiling its kernels)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the layer would shard by output columns or by K; see the design notes).", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(the layer would shard by output columns or by K).", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -611,6 +619,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     w.lib()
+    if args.attention_only:
+        print(json.dumps(bench_stream_attention(max(50, args.steps // 4))), flush=True)
+        return
     if args.sweep_only:
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
         print(json.dumps({"sweep": {"down_verify": bench_down_verify(ss, sw),

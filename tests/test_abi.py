@@ -171,3 +171,23 @@ def test_rmsnorm_quantize_rejections():
     assert f(None, fake, 1e-6, 4, 256, fake, fake, None) == w.W4A8_EINVAL
     assert f(fake, P((1 << 20) + 8), 1e-6, 4, 256, fake, fake, None) == w.W4A8_EINVAL  # misaligned gamma
     assert f(None, None, 1e-6, 0, 256, None, None, None) == w.W4A8_OK          # M == 0 is a no-op
+
+
+def test_stream_attention_rejections():
+    L = w.lib()
+    P = ctypes.c_void_p
+    fake = P(1 << 20)
+    f = L.w4a8_stream_attention
+    args = lambda H=4, Hkv=2, Nq=8, Nk=16, D=128, ws=None, wsb=0: (fake, fake, fake, fake, fake, fake, fake, 64, H, Hkv,
+                                                                   Nq, Nk, D, 0.1, fake, ws, wsb, None)
+    assert f(*args(D=64)) == w.W4A8_EUNSUPPORTED
+    assert f(*args(H=4, Hkv=3)) == w.W4A8_EINVAL          # H % Hkv
+    assert f(*args(Nk=0)) == w.W4A8_EINVAL
+    assert f(*args(Nq=1 << 23)) == w.W4A8_EINVAL          # beyond 32-bit row offsets
+    assert f(*args(Nq=0)) == w.W4A8_OK
+    # a shape that splits its key range needs the workspace
+    need = w.w4a8_stream_attention_workspace_bytes(32, 768, 3072)
+    assert need == 4 * 32 * 768 * (128 + 2) * 4
+    assert f(*args(H=32, Hkv=8, Nq=768, Nk=3072)) == w.W4A8_EINVAL
+    assert f(*args(H=32, Hkv=8, Nq=768, Nk=3072, ws=P((1 << 20) + 16), wsb=need)) == w.W4A8_EINVAL  # misaligned
+    assert w.w4a8_stream_attention_workspace_bytes(4, 64, 256) == 0

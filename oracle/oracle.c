@@ -12,8 +12,7 @@
  * backbone linear layer are cast to 8 bits, so the product runs on integer
  * hardware (Sec. 4.2, "Algorithm-level gains", reading Table 1: prefill gains
  * from the INT8 contraction, decode from the 4x smaller weight stream).  The paper fixes
- * no scale granularity, rounding or output precision; the readings used here
- * (each one listed with its reason in the design notes) are:
+ * no scale granularity, rounding or output precision; the readings used here are:
  *   - activations: per-token symmetric scale s = absmax/127 (fp32), codes
  *     q = clamp(round_half_even(x / s), -127, 127), an all-zero row has s = 0
  *     and q = 0;

@@ -5,7 +5,9 @@ by the CPU-baseline leg of bench.py, never by the product path.  It shares no
 code with the HIP sources.  The linear-layer functions follow FlashDrive
 Sec. 3.4 (4-bit weights, 8-bit activations, integer contraction) with the
 readings stated in oracle.c's header; silu_mul / gated follow Sec. 3.5
-(Kernel Fusion) with the SiLU reading stated in silu_mul.
+(Kernel Fusion) with the SiLU reading stated in silu_mul; rmsnorm_quantize
+follows Sec. 3.5 too, streaming_attention Sec. 3.1, and the flow_* functions
+(adaptive-step flow matching with its velocity cache) Sec. 3.3.
 """
 from __future__ import annotations
 
@@ -282,3 +284,91 @@ def rope_tables(P, D, base=10000.0):
     i = np.arange(D // 2, dtype=np.float64)
     ang = np.arange(P, dtype=np.float64)[:, None] * base ** (-2.0 * i / D)[None, :]
     return np.cos(ang).astype(np.float32), np.sin(ang).astype(np.float32)
+
+
+def flow_schedule(n_steps, n_reuse):
+    """Which steps of an n_steps flow-matching solve evaluate the velocity
+    network (True) and which reuse the cached velocity (False).
+
+    FlashDrive Sec. 3.3 (adaptive caching): the first few and the last few
+    steps are evaluated fresh, and n_reuse steps between them take the
+    velocity of the step before them, i.e. the last fresh one.  The paper
+    does not say how the fresh steps split between the two ends; this
+    oracle's reading splits them evenly, the odd one at the start: the first
+    ceil((n_steps - n_reuse) / 2) steps and the last floor((n_steps -
+    n_reuse) / 2) are fresh.  Step 0 is always fresh (1 <= n_steps, 0 <=
+    n_reuse < n_steps).  For the paper's 8 steps with 4 reused: steps 0, 1,
+    6 and 7 are fresh, 2 to 5 reuse step 1's velocity."""
+    if not (1 <= n_steps and 0 <= n_reuse < n_steps):
+        raise ValueError("flow_schedule needs 1 <= n_steps and 0 <= n_reuse < n_steps")
+    head = (n_steps - n_reuse + 1) // 2
+    return [i < head or i >= head + n_reuse for i in range(n_steps)]
+
+
+def flow_step(x, v_bits, cache_bits, dt):
+    """One explicit Euler step of the flow-matching ODE dx/dt = v (FlashDrive
+    Sec. 3.3), with the velocity cache.
+
+    x fp32 [B][n] (the trajectory state), v_bits the fresh velocity as bf16
+    bit patterns [B][n] (the action network's output) or None on a step
+    that reuses the cache, cache_bits bf16 [B][n] the cached velocity.
+    The update is x' = fl32(x + fl32(dt * v)), two fp32 IEEE operations
+    (no fused multiply-add), v being the fresh velocity or, on a reused
+    step, the cache.  A fresh step also replaces the cache by v and
+    returns, per row b, the four sums that give the consecutive-velocity
+    measures the paper plots for this section (relative difference and
+    cosine similarity, see flow_measures), taken against the cache before
+    the step:
+        stats[b] = (sum v c, sum v v, sum c c, sum (v - c)^2)
+    each term formed in fp64 from the bf16 values and the sum rounded once
+    (math.fsum).  Returns (x' fp32, cache' bf16 bits, stats fp64 [B][4] or
+    None)."""
+    import math
+
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    c_bits = np.ascontiguousarray(cache_bits, dtype=np.uint16)
+    dt32 = np.float32(dt)
+    if v_bits is None:
+        vel = _f32(c_bits)
+        return (x + dt32 * vel).astype(np.float32), c_bits.copy(), None
+    v_bits = np.ascontiguousarray(v_bits, dtype=np.uint16)
+    vel = _f32(v_bits)
+    B = x.shape[0]
+    v64 = vel.astype(np.float64).reshape(B, -1)
+    c64 = _f32(c_bits).astype(np.float64).reshape(B, -1)
+    stats = np.empty((B, 4))
+    for b in range(B):
+        d = v64[b] - c64[b]
+        stats[b] = (math.fsum(v64[b] * c64[b]), math.fsum(v64[b] * v64[b]),
+                    math.fsum(c64[b] * c64[b]), math.fsum(d * d))
+    return (x + dt32 * vel).astype(np.float32), v_bits.copy(), stats
+
+
+def flow_measures(stats):
+    """(relative difference ||v - c|| / ||c||, cosine similarity v.c / (||v|| ||c||))
+    per row of flow_step's stats; nan where a norm is zero."""
+    s = np.asarray(stats, dtype=np.float64)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        rel = np.sqrt(s[:, 3]) / np.sqrt(s[:, 2])
+        cos = s[:, 0] / np.sqrt(s[:, 1] * s[:, 2])
+    return rel, cos
+
+
+def flow_solve(x0, velocity, n_steps, n_reuse):
+    """The adaptive-step solve of FlashDrive Sec. 3.3 over t in [0, 1] with
+    uniform steps dt = 1 / n_steps: at step i (time t_i = i dt), a fresh
+    step calls velocity(x, t_i) -> bf16 bits [B][n] and updates the cache,
+    a reused one takes the cache (flow_schedule).  Returns (x after the last
+    step, list of per-step states, list of stats per fresh step)."""
+    fresh = flow_schedule(n_steps, n_reuse)
+    dt = np.float32(1.0) / np.float32(n_steps)
+    x = np.ascontiguousarray(x0, dtype=np.float32)
+    cache = np.zeros(x.shape, np.uint16)
+    states, stats = [], []
+    for i in range(n_steps):
+        v = velocity(x, i / n_steps) if fresh[i] else None
+        x, cache, st = flow_step(x, v, cache, dt)
+        states.append(x)
+        if st is not None:
+            stats.append(st)
+    return x, states, stats

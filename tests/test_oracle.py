@@ -572,3 +572,118 @@ def test_attention_of_constant_values_is_that_value():
     o, bnd = oracle.streaming_attention(q, k, v, np.array([5, 12, 19]), np.arange(Nk), cos_t, sin_t, 0.3)
     np.testing.assert_allclose(o, np.broadcast_to(f32_of_bits(row).astype(np.float64), o.shape), rtol=1e-13)
     np.testing.assert_allclose(bnd, np.abs(o), rtol=1e-13)
+
+
+# ---- adaptive-step flow matching with the velocity cache (Sec. 3.3)
+
+def test_flow_schedule_paper_case_and_shapes():
+    T, F = True, False
+    # 8 steps, 4 reused: the first two and the last two evaluated, the middle four reused
+    assert oracle.flow_schedule(8, 4) == [T, T, F, F, F, F, T, T]
+    assert oracle.flow_schedule(8, 0) == [T] * 8
+    assert oracle.flow_schedule(1, 0) == [T]
+    assert oracle.flow_schedule(5, 4) == [T, F, F, F, F]
+    assert oracle.flow_schedule(8, 3) == [T, T, T, F, F, F, T, T]
+    for n in range(1, 13):
+        for r in range(n):
+            s = oracle.flow_schedule(n, r)
+            assert len(s) == n and s[0] and s.count(False) == r
+            idx = [i for i, f in enumerate(s) if not f]
+            assert idx == list(range(idx[0], idx[0] + r)) if r else True  # one contiguous run
+            assert abs(s.index(False) - (n - 1 - idx[-1])) <= 1 if r else True  # centred
+    for bad in ((0, 0), (4, 4), (4, -1)):
+        with pytest.raises(ValueError):
+            oracle.flow_schedule(*bad)
+
+
+def test_flow_constant_field_integrates_exactly_under_any_schedule():
+    # dx/dt = c from t = 0 to 1 gives x0 + c; Euler is exact for a constant
+    # field, and a reused velocity equals the fresh one
+    x0 = np.full((2, 3), 0.5, np.float32)
+    for r in range(8):
+        x, _, _ = oracle.flow_solve(x0, lambda x, t: bits_of(np.full(x.shape, 0.75)), 8, r)
+        assert (x == np.float32(1.25)).all()
+
+
+def test_flow_time_field_closed_forms():
+    # dx/dt = 2t: fresh Euler sums 2 t_i dt = 1 - 1/n (all values dyadic, so exact)
+    vel = lambda x, t: bits_of(np.full(x.shape, 2.0 * t))
+    for n in (4, 8, 16):
+        x, _, _ = oracle.flow_solve(np.zeros((1, 2), np.float32), vel, n, 0)
+        assert (x == np.float32(1 - 1 / n)).all()
+    # 8 steps with 2-5 reused: the velocities taken are those of t = 0, 1/8
+    # (five times), 6/8 and 7/8 -> (0 + 5 * 0.25 + 1.5 + 1.75) / 8 = 0.5625
+    x, states, stats = oracle.flow_solve(np.zeros((1, 2), np.float32), vel, 8, 4)
+    assert (x == np.float32(0.5625)).all()
+    assert len(stats) == 4 and len(states) == 8
+    # a distinct constant per evaluation: 1 + 8t at t = 0, 1/8, 6/8, 7/8 -> (1 + 5 * 2 + 7 + 8) / 8
+    x, _, _ = oracle.flow_solve(np.zeros((1, 1), np.float32), lambda x, t: bits_of(np.full(x.shape, 1 + 8 * t)), 8, 4)
+    assert x[0, 0] == np.float32(3.25)
+
+
+def test_flow_step_stats_special_cases():
+    c = np.array([[3.0, 4.0]] * 5, np.float32)
+    v = np.array([[3.0, 4.0], [6.0, 8.0], [-3.0, -4.0], [4.0, -3.0], [0.0, 0.0]], np.float32)
+    x = np.zeros((5, 2), np.float32)
+    _, cache, st = oracle.flow_step(x, bits_of(v), bits_of(c), 0.125)
+    assert (cache == bits_of(v)).all()
+    # (v.c, v.v, c.c, |v - c|^2) by hand
+    assert st.tolist() == [[25, 25, 25, 0], [50, 100, 25, 25], [-25, 25, 25, 100], [0, 25, 25, 50], [0, 0, 25, 25]]
+    rel, cos = oracle.flow_measures(st)
+    assert rel[:4].tolist() == [0.0, 1.0, 2.0, math.sqrt(2.0)] and rel[4] == 1.0
+    assert cos[:4].tolist() == [1.0, 1.0, -1.0, 0.0] and np.isnan(cos[4])
+    # a reused step leaves the cache and returns no stats
+    x2, cache2, st2 = oracle.flow_step(x, None, bits_of(c), 0.5)
+    assert st2 is None and (cache2 == bits_of(c)).all() and (x2 == 0.5 * c).all()
+
+
+def test_flow_stats_match_exact_rational_sums():
+    r = rng(41)
+    v = bits_of(r.uniform(-4, 4, (3, 37)))
+    c = bits_of(r.uniform(-4, 4, (3, 37)))
+    _, _, st = oracle.flow_step(np.zeros((3, 37), np.float32), v, c, 0.25)
+    vf, cf = oracle._f32(v), oracle._f32(c)
+    for b in range(3):
+        V = [Fraction(float(a)) for a in vf[b]]
+        C = [Fraction(float(a)) for a in cf[b]]
+        want = (sum(a * e for a, e in zip(V, C)), sum(a * a for a in V), sum(e * e for e in C),
+                sum((a - e) ** 2 for a, e in zip(V, C)))
+        assert st[b].tolist() == [float(w) for w in want]
+
+
+def _round_f32(q: Fraction) -> float:
+    """Exact round-to-nearest-even of a rational to fp32 (normal range)."""
+    if q == 0:
+        return 0.0
+    s = -1 if q < 0 else 1
+    a = abs(q)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    while a >= Fraction(2) ** (e + 1):
+        e += 1
+    while a < Fraction(2) ** e:
+        e -= 1
+    m = a / Fraction(2) ** (e - 23)                 # in [2^23, 2^24)
+    fl = m.numerator // m.denominator
+    rem = m - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2):
+        fl += 1
+    return s * float(Fraction(fl) * Fraction(2) ** (e - 23))
+
+
+def test_flow_update_rounds_the_product_then_the_sum():
+    # x' = fl32(x + fl32(dt v)): checked with exact rational arithmetic; the
+    # fused form fl32(x + dt v) differs on some of these inputs
+    r = rng(42)
+    x = r.uniform(-2, 2, (1, 400)).astype(np.float32)
+    v = bits_of(r.uniform(-4, 4, (1, 400)))
+    dt = np.float32(0.1)
+    out, _, _ = oracle.flow_step(x, v, v, dt)
+    vf = oracle._f32(v)
+    differ = 0
+    for i in range(400):
+        p = _round_f32(Fraction(float(dt)) * Fraction(float(vf[0, i])))
+        want = _round_f32(Fraction(float(x[0, i])) + Fraction(p))
+        fused = _round_f32(Fraction(float(x[0, i])) + Fraction(float(dt)) * Fraction(float(vf[0, i])))
+        assert float(out[0, i]) == want
+        differ += fused != want
+    assert differ > 0

@@ -440,6 +440,66 @@ def bench_stream_attention(steps):
             "frac_bf16": round(tflops / BF16_PEAK_TFLOPS, 4)}
 
 
+def bench_flow(steps):
+    """The flow-matching Euler step with the velocity cache (w4a8_flow_step),
+    graph-replayed.  The paper's shape: 6 trajectory samples x 64 waypoints
+    x 2 values, launch-bound; per step and for the 8-step solve with 4
+    steps reused (4 evaluated steps with their row sums, 4 reused; the
+    action network itself is not part of this library).  The bandwidth
+    shape, 16384 x 2048: algorithmic bytes 14 per element on an evaluated
+    step (x read and written, v read, cache read and written), 10 on a
+    reused one (x read and written, cache read)."""
+    import torch
+    import paper_2608_12932_amd as w
+    from paper_2608_12932_amd import inputs as I
+
+    L = w.lib()
+    dev = torch.device("cuda:0")
+    out = {}
+    for label, B, n in (("paper", 6, 128), ("bandwidth", 16384, 2048)):
+        x = torch.from_numpy(I.flow_state(B, n, 61)).to(dev)
+        bf = lambda bits: torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
+        v = bf(I.flow_velocity(B, n, 62))
+        c = bf(I.flow_velocity(B, n, 63))
+        st = torch.empty((B, 4), dtype=torch.float64, device=dev)
+        # a device copy of known size (B n 2 bytes read and written), the
+        # calibration of the HBM byte counters in a profiled run
+        calib = v.clone()
+        xp, vp, cp, sp = x.data_ptr(), v.data_ptr(), c.data_ptr(), st.data_ptr()
+        dt = 0.125
+
+        def fresh(i, stream):
+            if L.w4a8_flow_step(xp, vp, cp, B, n, dt, sp, stream):
+                raise RuntimeError("w4a8_flow_step failed")
+
+        def reuse(i, stream):
+            if L.w4a8_flow_step(xp, None, cp, B, n, dt, None, stream):
+                raise RuntimeError("w4a8_flow_step failed")
+
+        sched = w.w4a8_flow_schedule(8, 4)
+
+        def solve(i, stream):
+            for f in sched:
+                (fresh if f else reuse)(i, stream)
+
+        t_f = graph_ms(fresh, steps) * 1e3
+        t_r = graph_ms(reuse, steps) * 1e3
+        row = {"B": B, "n": n, "us_evaluated_step": round(t_f, 3), "us_reused_step": round(t_r, 3)}
+        if label == "paper":
+            row["us_solve_8_steps_4_reused"] = round(graph_ms(solve, max(10, steps // 8), reps=5) * 1e3, 3)
+            row["network_evaluations"] = {"cached": sum(sched), "uncached": len(sched)}
+        else:
+            ef, er = 14 * B * n, 10 * B * n
+            row.update({"GB/s_evaluated": round(ef / (t_f * 1e-6) / 1e9, 1),
+                        "GB/s_reused": round(er / (t_r * 1e-6) / 1e9, 1),
+                        "frac_hbm_evaluated": round(ef / (t_f * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                        "algorithmic_bytes_evaluated": ef, "algorithmic_bytes_reused": er})
+        out[label] = row
+        del x, v, c, st, calib
+    torch.cuda.empty_cache()
+    return {"workload": "flow-matching Euler step with the velocity cache, graph-replayed", **out}
+
+
 def bench_layer_group(steps, warmup, copies=6):
     """One decoder layer's four linears (QKV, O, gate+up, down) with group-128
     fp16 scales; a step is the four calls, each on its own bf16 x.  Six copies
@@ -608,6 +668,8 @@ def main():
                     help="run only the sweeps (for profiling their kernels); prints the sweep object")
     ap.add_argument("--attention-only", action="store_true",
                     help="run only the streaming attention workload (for profiling its kernels)")
+    ap.add_argument("--flow-only", action="store_true",
+                    help="run only the flow-matching step workloads (for profiling their kernel)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
@@ -622,12 +684,16 @@ def main():
     if args.attention_only:
         print(json.dumps(bench_stream_attention(max(50, args.steps // 4))), flush=True)
         return
+    if args.flow_only:
+        print(json.dumps(bench_flow(max(50, args.steps // 4))), flush=True)
+        return
     if args.sweep_only:
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
         print(json.dumps({"sweep": {"down_verify": bench_down_verify(ss, sw),
                                     "gate_up_swiglu": bench_gate_up_swiglu(ss, sw),
                                     "rmsnorm_prologue": bench_rmsnorm_prologue(ss),
                                     "stream_attention": bench_stream_attention(ss),
+                                    "flow_step": bench_flow(ss),
                                     "layer_group": bench_layer_group(ss, sw),
                                     "stack": bench_stack(max(10, args.steps // 50))}}), flush=True)
         return
@@ -683,6 +749,7 @@ def main():
         out["sweep"] = {"down_verify": bench_down_verify(ss, sw), "gate_up_swiglu": bench_gate_up_swiglu(ss, sw),
                         "rmsnorm_prologue": bench_rmsnorm_prologue(ss),
                         "stream_attention": bench_stream_attention(ss),
+                        "flow_step": bench_flow(ss),
                         "layer_group": bench_layer_group(ss, sw),
                         "stack": bench_stack(max(10, args.steps // 50))}
     if not args.no_cpu_baseline:

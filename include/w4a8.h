@@ -270,6 +270,53 @@ size_t w4a8_linear_swiglu_workspace_bytes(int64_t M, int64_t N, int64_t K, int s
 /* The kernels w4a8_linear_swiglu would use, as w4a8_linear_describe. */
 const char* w4a8_linear_swiglu_describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind);
 
+/*
+ * Which steps of an n_steps flow-matching solve evaluate the action network
+ * and which reuse the cached velocity.  FlashDrive, Sec. 3.3 ("Adaptive
+ * caching"): the first few and the last few steps are evaluated, and
+ * n_reuse steps between them take the velocity of the last evaluated step.
+ * The paper leaves the split of the evaluated steps between the two ends
+ * open; this library's reading splits them evenly, the odd one at the
+ * start: steps i < h and i >= h + n_reuse are evaluated, h = ceil((n_steps
+ * - n_reuse) / 2).  The paper's 8 steps with 4 reused give 1 1 0 0 0 0 1 1.
+ *   n_steps  1 <= n_steps <= 4096
+ *   n_reuse  0 <= n_reuse < n_steps (step 0 is always evaluated)
+ *   fresh    host, int32 [n_steps]: 1 evaluate, 0 reuse
+ * Host-only: touches no device.
+ */
+w4a8_status w4a8_flow_schedule(int64_t n_steps, int64_t n_reuse, int32_t* fresh);
+
+/*
+ * One explicit Euler step x <- x + dt v of the flow-matching ODE of the
+ * action head, with the velocity cache (FlashDrive, Sec. 3.3).  The action
+ * network stays outside this library (the paper keeps it in BF16); its
+ * velocity output is the input here.
+ *   - Evaluated step (v_new != NULL): x[b,i] = fl32(x[b,i] + fl32(dt v_new[b,i])),
+ *     then v_cache = v_new; with stats != NULL, per row b the sums behind
+ *     the consecutive-velocity relative difference ||v - c|| / ||c|| and
+ *     cosine v.c / (||v|| ||c||) that motivate the reuse, against the cache
+ *     c before the step:
+ *         stats[b] = (sum_i v c, sum_i v v, sum_i c c, sum_i (v - c)^2)
+ *     each term formed in fp64 (exact for the products), summed in fp64
+ *     in an unspecified order.
+ *   - Reused step (v_new == NULL): x[b,i] = fl32(x[b,i] + fl32(dt v_cache[b,i]));
+ *     the cache is unchanged, and stats must be NULL.
+ * Both fp32 operations are rounded separately (no fused multiply-add), so
+ * x and the cache are bit-exact functions of the inputs.
+ *   x        device, fp32 [B][n] trajectory state, 16-byte aligned, updated in place
+ *   v_new    device, bf16 [B][n] or NULL, 16-byte aligned
+ *   v_cache  device, bf16 [B][n], 16-byte aligned (v_new may equal it;
+ *            no other overlap among x, v_new and v_cache is allowed)
+ *   B, n     0 <= B <= 2^24 (0 is a no-op), 1 <= n <= 2^26
+ *   dt       finite (1 / n_steps for uniform steps)
+ *   stats    device, fp64 [B][4] or NULL, 8-byte aligned
+ * Does not synchronize.  One workgroup per row: rows of thousands of
+ * elements and more reach HBM rates, the paper's trajectories (a few
+ * hundred values per sample) are launch-bound.
+ */
+w4a8_status w4a8_flow_step(float* x, const uint16_t* v_new, uint16_t* v_cache, int64_t B, int64_t n, float dt,
+                           double* stats, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -27,7 +27,7 @@ EXPORTS = ("w4a8_status_string", "w4a8_packed_weight_bytes", "w4a8_pack_weights"
            "w4a8_quantize_act", "w4a8_linear_workspace_bytes", "w4a8_linear",
            "w4a8_linear_describe", "w4a8_linear_swiglu", "w4a8_linear_swiglu_workspace_bytes",
            "w4a8_linear_swiglu_describe", "w4a8_rmsnorm_quantize_act", "w4a8_stream_attention",
-           "w4a8_stream_attention_workspace_bytes")
+           "w4a8_stream_attention_workspace_bytes", "w4a8_flow_schedule", "w4a8_flow_step")
 
 _OUT_DTYPE = {OUT_BF16: torch.bfloat16, OUT_F32: torch.float32, OUT_I32_ACC: torch.int32}
 
@@ -65,6 +65,10 @@ def lib() -> ctypes.CDLL:
         L.w4a8_stream_attention.restype = I
         L.w4a8_stream_attention_workspace_bytes.argtypes = [I64, I64, I64]
         L.w4a8_stream_attention_workspace_bytes.restype = SZ
+        L.w4a8_flow_schedule.argtypes = [I64, I64, P]
+        L.w4a8_flow_schedule.restype = I
+        L.w4a8_flow_step.argtypes = [P, P, P, I64, I64, ctypes.c_float, P, P]
+        L.w4a8_flow_step.restype = I
         L.w4a8_linear_workspace_bytes.argtypes = [I64, I64, I64, I, I]
         L.w4a8_linear_workspace_bytes.restype = SZ
         L.w4a8_linear.argtypes = [P, I, P, I64, I64, P, P, I, I64, P, I, P, SZ, P]
@@ -150,6 +154,36 @@ def w4a8_rmsnorm_quantize_act(x: torch.Tensor, gamma: torch.Tensor, eps: float, 
     rc = lib().w4a8_rmsnorm_quantize_act(x_ptr, g_ptr, float(eps), M, K, q.data_ptr(), s.data_ptr(), _stream(stream))
     _check(rc, "w4a8_rmsnorm_quantize_act")
     return q, s
+
+
+def w4a8_flow_schedule(n_steps: int, n_reuse: int) -> list:
+    """Per step of an n_steps flow-matching solve: True where the action
+    network is evaluated, False where the cached velocity is reused."""
+    import ctypes
+
+    buf = (ctypes.c_int32 * max(int(n_steps), 1))()
+    _check(lib().w4a8_flow_schedule(n_steps, n_reuse, buf), "w4a8_flow_schedule")
+    return [bool(buf[i]) for i in range(n_steps)]
+
+
+def w4a8_flow_step(x: torch.Tensor, v_new, v_cache: torch.Tensor, dt: float, stats: bool = False, stream=None):
+    """Euler step x += dt v of the flow-matching solve, in place on fp32 x
+    [B][n].  v_new bf16 [B][n] (an evaluated step: the cache becomes v_new)
+    or None (a reused step: v = v_cache).  With stats (evaluated steps
+    only) returns fp64 [B][4] = (v.c, v.v, c.c, |v - c|^2) against the
+    cache before the step, else None."""
+    B, n = x.shape
+    x_ptr = _dev(x, "x", torch.float32)
+    c_ptr = _dev(v_cache, "v_cache", torch.bfloat16)
+    v_ptr = None if v_new is None else _dev(v_new, "v_new", torch.bfloat16)
+    for name, t in (("v_cache", v_cache), ("v_new", v_new)):
+        if t is not None and tuple(t.shape) != (B, n):
+            raise ValueError(f"{name} must be [{B}][{n}]")
+    st = torch.empty((B, 4), dtype=torch.float64, device=x.device) if stats else None
+    rc = lib().w4a8_flow_step(x_ptr, v_ptr, c_ptr, B, n, float(dt), None if st is None else st.data_ptr(),
+                              _stream(stream))
+    _check(rc, "w4a8_flow_step")
+    return st
 
 
 def w4a8_linear_workspace_bytes(M: int, N: int, K: int, scale_mode: int = SCALE_CHANNEL_F32,

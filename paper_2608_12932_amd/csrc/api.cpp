@@ -228,6 +228,38 @@ w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, 
                                                                                                   : W4A8_EHIP;
 }
 
+w4a8_status w4a8_flow_schedule(int64_t n_steps, int64_t n_reuse, int32_t* fresh) {
+  if (n_steps < 1 || n_steps > 4096 || n_reuse < 0 || n_reuse >= n_steps || !fresh) return W4A8_EINVAL;
+  const int64_t head = (n_steps - n_reuse + 1) / 2;
+  for (int64_t i = 0; i < n_steps; ++i) fresh[i] = (i < head || i >= head + n_reuse) ? 1 : 0;
+  return W4A8_OK;
+}
+
+w4a8_status w4a8_flow_step(float* x, const uint16_t* v_new, uint16_t* v_cache, int64_t B, int64_t n, float dt,
+                           double* stats, hipStream_t stream) {
+  if (B < 0 || B > (int64_t(1) << 24) || n < 1 || n > (int64_t(1) << 26)) return W4A8_EINVAL;
+  if (!(dt == dt) || dt > 3.4e38f || dt < -3.4e38f) return W4A8_EINVAL;  // finite
+  if (!v_new && stats) return W4A8_EINVAL;
+  if (B == 0) return W4A8_OK;
+  if (!x || !v_cache || !aligned(x, 16) || !aligned(v_cache, 16) || (v_new && !aligned(v_new, 16)) ||
+      (stats && !aligned(stats, 8)))
+    return W4A8_EINVAL;
+  const uintptr_t xs = reinterpret_cast<uintptr_t>(x), cs = reinterpret_cast<uintptr_t>(v_cache);
+  const uintptr_t xb = uintptr_t(B * n * 4), hb = uintptr_t(B * n * 2);
+  auto overlap = [](uintptr_t a, uintptr_t na, uintptr_t b, uintptr_t nb) { return a < b + nb && b < a + na; };
+  if (overlap(xs, xb, cs, hb)) return W4A8_EINVAL;
+  if (v_new) {
+    const uintptr_t vs = reinterpret_cast<uintptr_t>(v_new);
+    if (overlap(xs, xb, vs, hb) || (vs != cs && overlap(vs, hb, cs, hb))) return W4A8_EINVAL;
+    if (stats) {
+      const uintptr_t ss = reinterpret_cast<uintptr_t>(stats), sb = uintptr_t(B * 32);
+      if (overlap(ss, sb, xs, xb) || overlap(ss, sb, vs, hb) || overlap(ss, sb, cs, hb)) return W4A8_EINVAL;
+    }
+  }
+  return launch_flow_step(x, v_new, v_cache, (int)B, (int)n, dt, stats, stream) == hipSuccess ? W4A8_OK
+                                                                                               : W4A8_EHIP;
+}
+
 size_t w4a8_stream_attention_workspace_bytes(int64_t H, int64_t Nq, int64_t Nk) {
   constexpr int64_t kMax = int64_t(1) << 22;
   if (H < 1 || H > 4096 || Nq < 1 || Nq > kMax || Nk < 1 || Nk > kMax) return 0;

@@ -52,6 +52,11 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) { return __builtin_bit_ca
 // position pos, as bf16 words: lo = a cos - b sin, hi = b cos + a sin.
 __device__ __forceinline__ void rotate_chunks(uint4 a8, uint4 b8, const float* cs, const float* sn, uint4& lo,
                                               uint4& hi) {
+  // three roundings per output (two products, then the sum), as in plain
+  // fp32 arithmetic: no contraction into fused multiply-adds (the _rn
+  // intrinsics are ordinary operators in their own scope and would be
+  // contracted)
+#pragma clang fp contract(off)
   const uint32_t aw[4] = {a8.x, a8.y, a8.z, a8.w}, bw[4] = {b8.x, b8.y, b8.z, b8.w};
   uint32_t lw[4], hw[4];
 #pragma unroll
@@ -59,8 +64,8 @@ __device__ __forceinline__ void rotate_chunks(uint4 a8, uint4 b8, const float* c
     const float a0 = bf16_lo(aw[e]), a1 = bf16_hi(aw[e]);
     const float b0 = bf16_lo(bw[e]), b1 = bf16_hi(bw[e]);
     const float c0 = cs[2 * e], c1 = cs[2 * e + 1], s0 = sn[2 * e], s1 = sn[2 * e + 1];
-    lw[e] = bf16x2_bits(__fsub_rn(__fmul_rn(a0, c0), __fmul_rn(b0, s0)), __fsub_rn(__fmul_rn(a1, c1), __fmul_rn(b1, s1)));
-    hw[e] = bf16x2_bits(__fadd_rn(__fmul_rn(b0, c0), __fmul_rn(a0, s0)), __fadd_rn(__fmul_rn(b1, c1), __fmul_rn(a1, s1)));
+    lw[e] = bf16x2_bits(a0 * c0 - b0 * s0, a1 * c1 - b1 * s1);
+    hw[e] = bf16x2_bits(b0 * c0 + a0 * s0, b1 * c1 + a1 * s1);
   }
   lo = make_uint4(lw[0], lw[1], lw[2], lw[3]);
   hi = make_uint4(hw[0], hw[1], hw[2], hw[3]);

@@ -112,3 +112,17 @@ def workload_inputs(key: str, M: int, layer: int = 0, mat_index: int = 0):
     x = activations(M, K, seed_x(wl.number, M), wl.outliers)
     W, s = weights(N, K, seed_w(wl.number, layer, name), wl.group)
     return x, W, s, K, N
+
+
+def flow_state(B: int, n: int, seed: int) -> np.ndarray:
+    """fp32 [B][n] start of a flow-matching solve: N(0, 1) noise, the prior
+    the action head denoises from (B trajectory samples of n values)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return rng.standard_normal((B, n), dtype=np.float32)
+
+
+def flow_velocity(B: int, n: int, seed: int, scale: float = 2.0) -> np.ndarray:
+    """bf16 bit patterns [B][n]: a stand-in for the action network's velocity
+    output, N(0, scale^2) rounded to bf16."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return to_bf16_bits(rng.standard_normal((B, n), dtype=np.float32) * np.float32(scale))

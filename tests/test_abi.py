@@ -191,3 +191,36 @@ def test_stream_attention_rejections():
     assert f(*args(H=32, Hkv=8, Nq=768, Nk=3072)) == w.W4A8_EINVAL
     assert f(*args(H=32, Hkv=8, Nq=768, Nk=3072, ws=P((1 << 20) + 16), wsb=need)) == w.W4A8_EINVAL  # misaligned
     assert w.w4a8_stream_attention_workspace_bytes(4, 64, 256) == 0
+
+
+def test_flow_schedule_matches_the_oracle_reading():
+    import oracle
+
+    assert w.w4a8_flow_schedule(8, 4) == [True, True, False, False, False, False, True, True]
+    for n in range(1, 17):
+        for r in range(n):
+            assert w.w4a8_flow_schedule(n, r) == oracle.flow_schedule(n, r), (n, r)
+    L = w.lib()
+    buf = (ctypes.c_int32 * 8)()
+    for bad in ((0, 0), (8, 8), (8, -1), (4097, 0)):
+        assert L.w4a8_flow_schedule(*bad, buf) == w.W4A8_EINVAL
+    assert L.w4a8_flow_schedule(8, 4, None) == w.W4A8_EINVAL
+
+
+def test_flow_step_rejections():
+    L = w.lib()
+    P = ctypes.c_void_p
+    X, V, C, S = P(1 << 24), P(2 << 24), P(3 << 24), P(4 << 24)  # disjoint fake addresses
+    f = L.w4a8_flow_step
+    assert f(X, None, C, 6, 128, 0.125, S, None) == w.W4A8_EINVAL      # stats on a reused step
+    assert f(X, V, C, 6, 0, 0.125, None, None) == w.W4A8_EINVAL        # n >= 1
+    assert f(X, V, C, -1, 8, 0.125, None, None) == w.W4A8_EINVAL
+    assert f(X, V, C, (1 << 24) + 1, 8, 0.125, None, None) == w.W4A8_EINVAL
+    assert f(X, V, C, 6, 128, float("inf"), None, None) == w.W4A8_EINVAL
+    assert f(X, V, C, 6, 128, float("nan"), None, None) == w.W4A8_EINVAL
+    assert f(P((1 << 24) + 4), V, C, 6, 128, 0.125, None, None) == w.W4A8_EINVAL   # misaligned x
+    assert f(X, V, C, 6, 128, 0.125, P((4 << 24) + 4), None) == w.W4A8_EINVAL      # misaligned stats
+    assert f(X, V, P((1 << 24) + 1024), 6, 128, 0.125, None, None) == w.W4A8_EINVAL  # cache inside x
+    assert f(X, P((3 << 24) + 16), C, 6, 128, 0.125, None, None) == w.W4A8_EINVAL   # v_new straddles the cache
+    assert f(X, V, C, 6, 128, 0.125, P((2 << 24) + 64), None) == w.W4A8_EINVAL      # stats inside v_new
+    assert f(None, None, None, 0, 128, 0.125, None, None) == w.W4A8_OK               # B == 0 is a no-op

@@ -332,14 +332,18 @@ __global__ __launch_bounds__(256) void attn_combine(const AttnArgs a) {
 
 }  // namespace
 
-// Key-range splits: enough workgroups to fill the chip about four times over
-// (at most 8 splits, at least 8 tiles each); the heaviest workgroups, whose
-// queries see the whole window, otherwise run every tile in series.
+// Key-range splits (at most 8, at least 8 tiles each): the heaviest
+// workgroups, whose queries see the whole window, otherwise run every tile
+// in series.
 int stream_attention_splits(int H, int Nq, int Nk) {
   const long blocks = (long)((Nq + kQPerBlock - 1) / kQPerBlock) * H;
   const int ntiles = (Nk + kKeys - 1) / kKeys;
+  // split until the grid would outgrow one round of resident workgroups
+  // (3 per CU, bound by the kernel's 160 registers per lane, on 256 CUs):
+  // a second round costs more than the longer serial key loop it saves
+  constexpr long kResident = 3 * 256;
   int S = 1;
-  while (S < 8 && blocks * S * 2 <= 2048 && ntiles / (S * 2) >= 8) S *= 2;
+  while (S < 8 && blocks * S * 2 <= kResident && ntiles / (S * 2) >= 8) S *= 2;
   return S;
 }
 

@@ -75,7 +75,10 @@ __device__ __forceinline__ void rotate_chunks(uint4 a8, uint4 b8, const float* c
 // count are never skipped).
 constexpr int kMaxSkipTiles = 512;
 
-__global__ __launch_bounds__(kAttnWaves * 64) void stream_attention(const AttnArgs a) {
+// The occupancy hint (4 workgroups, i.e. 4 waves per SIMD) holds the kernel
+// to 128 registers; the few it spills are prologue values reloaded after the
+// key loop, which runs without scratch traffic.
+__global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const AttnArgs a) {
   // two stages of the key / value tile: the next visible tile is staged
   // while the current one is computed
   __shared__ __align__(16) uint16_t l_k[2][kKeys * kKPitch];     // rotated keys [key][d]
@@ -339,9 +342,9 @@ int stream_attention_splits(int H, int Nq, int Nk) {
   const long blocks = (long)((Nq + kQPerBlock - 1) / kQPerBlock) * H;
   const int ntiles = (Nk + kKeys - 1) / kKeys;
   // split until the grid would outgrow one round of resident workgroups
-  // (3 per CU, bound by the kernel's 160 registers per lane, on 256 CUs):
-  // a second round costs more than the longer serial key loop it saves
-  constexpr long kResident = 3 * 256;
+  // (4 per CU at 128 registers per lane, on 256 CUs): a second round costs
+  // more than the longer serial key loop it saves
+  constexpr long kResident = 4 * 256;
   int S = 1;
   while (S < 8 && blocks * S * 2 <= kResident && ntiles / (S * 2) >= 8) S *= 2;
   return S;

@@ -468,27 +468,44 @@ def bench_flow(steps):
         xp, vp, cp, sp = x.data_ptr(), v.data_ptr(), c.data_ptr(), st.data_ptr()
         dt = 0.125
 
-        def fresh(i, stream):
-            if L.w4a8_flow_step(xp, vp, cp, B, n, dt, sp, stream):
+        def fresh(i, stream, repeat=1):
+            if L.w4a8_flow_step(xp, vp, cp, B, n, dt, repeat, sp, stream):
                 raise RuntimeError("w4a8_flow_step failed")
 
         def reuse(i, stream):
-            if L.w4a8_flow_step(xp, None, cp, B, n, dt, None, stream):
+            if L.w4a8_flow_step(xp, None, cp, B, n, dt, 1, None, stream):
                 raise RuntimeError("w4a8_flow_step failed")
 
         sched = w.w4a8_flow_schedule(8, 4)
+        # one call per evaluated step, the reused steps after it folded in
+        runs = []
+        for f in sched:
+            if f:
+                runs.append(1)
+            else:
+                runs[-1] += 1
 
         def solve(i, stream):
             for f in sched:
                 (fresh if f else reuse)(i, stream)
+
+        def solve_runs(i, stream):
+            for r in runs:
+                fresh(i, stream, r)
 
         t_f = graph_ms(fresh, steps) * 1e3
         t_r = graph_ms(reuse, steps) * 1e3
         row = {"B": B, "n": n, "us_evaluated_step": round(t_f, 3), "us_reused_step": round(t_r, 3)}
         if label == "paper":
             row["us_solve_8_steps_4_reused"] = round(graph_ms(solve, max(10, steps // 8), reps=5) * 1e3, 3)
+            row["us_solve_folded_runs"] = round(graph_ms(solve_runs, max(10, steps // 8), reps=5) * 1e3, 3)
+            row["calls_folded"] = len(runs)
             row["network_evaluations"] = {"cached": sum(sched), "uncached": len(sched)}
         else:
+            # the folded run of an evaluated step with its 4 reused steps: 14 bytes per element, one pass
+            t_5 = graph_ms(lambda i, st_: fresh(i, st_, 5), steps) * 1e3
+            row["us_evaluated_plus_4_reused_folded"] = round(t_5, 3)
+            row["us_evaluated_plus_4_reused_separate"] = round(t_f + 4 * t_r, 3)
             ef, er = 14 * B * n, 10 * B * n
             row.update({"GB/s_evaluated": round(ef / (t_f * 1e-6) / 1e9, 1),
                         "GB/s_reused": round(er / (t_r * 1e-6) / 1e9, 1),

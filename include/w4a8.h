@@ -303,19 +303,26 @@ w4a8_status w4a8_flow_schedule(int64_t n_steps, int64_t n_reuse, int32_t* fresh)
  *     the cache is unchanged, and stats must be NULL.
  * Both fp32 operations are rounded separately (no fused multiply-add), so
  * x and the cache are bit-exact functions of the inputs.
+ * `repeat` applies the update that many times in the one call, each
+ * rounded as a separate step: an evaluated step and the reused steps that
+ * follow it (all with its velocity) take one call with repeat = 1 + the
+ * number of reused steps, giving the bits of the step-by-step calls with
+ * one pass over x.  The schedule 1 1 0 0 0 0 1 1 becomes four calls with
+ * repeat 1, 5, 1, 1.
  *   x        device, fp32 [B][n] trajectory state, 16-byte aligned, updated in place
  *   v_new    device, bf16 [B][n] or NULL, 16-byte aligned
  *   v_cache  device, bf16 [B][n], 16-byte aligned (v_new may equal it;
  *            no other overlap among x, v_new and v_cache is allowed)
  *   B, n     0 <= B <= 2^24 (0 is a no-op), 1 <= n <= 2^26
  *   dt       finite (1 / n_steps for uniform steps)
+ *   repeat   1 <= repeat <= 4096
  *   stats    device, fp64 [B][4] or NULL, 8-byte aligned
  * Does not synchronize.  One workgroup per row: rows of thousands of
  * elements and more reach HBM rates, the paper's trajectories (a few
  * hundred values per sample) are launch-bound.
  */
 w4a8_status w4a8_flow_step(float* x, const uint16_t* v_new, uint16_t* v_cache, int64_t B, int64_t n, float dt,
-                           double* stats, hipStream_t stream);
+                           int64_t repeat, double* stats, hipStream_t stream);
 
 #ifdef __cplusplus
 }

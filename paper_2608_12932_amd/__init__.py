@@ -67,7 +67,7 @@ def lib() -> ctypes.CDLL:
         L.w4a8_stream_attention_workspace_bytes.restype = SZ
         L.w4a8_flow_schedule.argtypes = [I64, I64, P]
         L.w4a8_flow_schedule.restype = I
-        L.w4a8_flow_step.argtypes = [P, P, P, I64, I64, ctypes.c_float, P, P]
+        L.w4a8_flow_step.argtypes = [P, P, P, I64, I64, ctypes.c_float, I64, P, P]
         L.w4a8_flow_step.restype = I
         L.w4a8_linear_workspace_bytes.argtypes = [I64, I64, I64, I, I]
         L.w4a8_linear_workspace_bytes.restype = SZ
@@ -166,12 +166,14 @@ def w4a8_flow_schedule(n_steps: int, n_reuse: int) -> list:
     return [bool(buf[i]) for i in range(n_steps)]
 
 
-def w4a8_flow_step(x: torch.Tensor, v_new, v_cache: torch.Tensor, dt: float, stats: bool = False, stream=None):
+def w4a8_flow_step(x: torch.Tensor, v_new, v_cache: torch.Tensor, dt: float, stats: bool = False, stream=None,
+                   repeat: int = 1):
     """Euler step x += dt v of the flow-matching solve, in place on fp32 x
-    [B][n].  v_new bf16 [B][n] (an evaluated step: the cache becomes v_new)
-    or None (a reused step: v = v_cache).  With stats (evaluated steps
-    only) returns fp64 [B][4] = (v.c, v.v, c.c, |v - c|^2) against the
-    cache before the step, else None."""
+    [B][n], applied `repeat` times (consecutive steps with the same
+    velocity).  v_new bf16 [B][n] (an evaluated step: the cache becomes
+    v_new) or None (a reused step: v = v_cache).  With stats (evaluated
+    steps only) returns fp64 [B][4] = (v.c, v.v, c.c, |v - c|^2) against
+    the cache before the step, else None."""
     B, n = x.shape
     x_ptr = _dev(x, "x", torch.float32)
     c_ptr = _dev(v_cache, "v_cache", torch.bfloat16)
@@ -180,8 +182,8 @@ def w4a8_flow_step(x: torch.Tensor, v_new, v_cache: torch.Tensor, dt: float, sta
         if t is not None and tuple(t.shape) != (B, n):
             raise ValueError(f"{name} must be [{B}][{n}]")
     st = torch.empty((B, 4), dtype=torch.float64, device=x.device) if stats else None
-    rc = lib().w4a8_flow_step(x_ptr, v_ptr, c_ptr, B, n, float(dt), None if st is None else st.data_ptr(),
-                              _stream(stream))
+    rc = lib().w4a8_flow_step(x_ptr, v_ptr, c_ptr, B, n, float(dt), int(repeat),
+                              None if st is None else st.data_ptr(), _stream(stream))
     _check(rc, "w4a8_flow_step")
     return st
 

@@ -236,8 +236,9 @@ w4a8_status w4a8_flow_schedule(int64_t n_steps, int64_t n_reuse, int32_t* fresh)
 }
 
 w4a8_status w4a8_flow_step(float* x, const uint16_t* v_new, uint16_t* v_cache, int64_t B, int64_t n, float dt,
-                           double* stats, hipStream_t stream) {
+                           int64_t repeat, double* stats, hipStream_t stream) {
   if (B < 0 || B > (int64_t(1) << 24) || n < 1 || n > (int64_t(1) << 26)) return W4A8_EINVAL;
+  if (repeat < 1 || repeat > 4096) return W4A8_EINVAL;
   if (!(dt == dt) || dt > 3.4e38f || dt < -3.4e38f) return W4A8_EINVAL;  // finite
   if (!v_new && stats) return W4A8_EINVAL;
   if (B == 0) return W4A8_OK;
@@ -256,8 +257,9 @@ w4a8_status w4a8_flow_step(float* x, const uint16_t* v_new, uint16_t* v_cache, i
       if (overlap(ss, sb, xs, xb) || overlap(ss, sb, vs, hb) || overlap(ss, sb, cs, hb)) return W4A8_EINVAL;
     }
   }
-  return launch_flow_step(x, v_new, v_cache, (int)B, (int)n, dt, stats, stream) == hipSuccess ? W4A8_OK
-                                                                                               : W4A8_EHIP;
+  return launch_flow_step(x, v_new, v_cache, (int)B, (int)n, dt, (int)repeat, stats, stream) == hipSuccess
+             ? W4A8_OK
+             : W4A8_EHIP;
 }
 
 size_t w4a8_stream_attention_workspace_bytes(int64_t H, int64_t Nq, int64_t Nk) {

@@ -9,6 +9,10 @@
 // compared with the new velocity (the four row sums behind the
 // consecutive-velocity relative difference and cosine similarity).
 //
+// A call may apply several consecutive steps with the same velocity: an
+// evaluated step and the reused steps after it take one launch and one
+// pass over the state, with the roundings of separate steps.
+//
 // One workgroup of 256 threads per row; with n % 8 == 0 each thread moves 8
 // elements per pass as 16-byte loads and stores, otherwise one.  The row
 // sums are fp64: the products of two bf16 values are exact there.  v may be
@@ -39,16 +43,18 @@ __device__ __forceinline__ double wave_sum(double s) {
   return s;
 }
 
-// x' = fl32(x + fl32(dt v)), no contraction into a fused multiply-add
-__device__ __forceinline__ float euler(float x, float dt, float v) {
+// x' = fl32(x + fl32(dt v)) applied `repeat` times, no contraction into a
+// fused multiply-add
+__device__ __forceinline__ float euler(float x, float dt, float v, int repeat) {
 #pragma clang fp contract(off)
   const float p = dt * v;
-  return x + p;
+  for (int r = 0; r < repeat; ++r) x = x + p;
+  return x;
 }
 
 template <bool FRESH, bool STATS, bool VEC>
 __global__ __launch_bounds__(kFlowThreads) void flow_step_rows(float* __restrict__ x, const uint16_t* v,
-                                                               uint16_t* cache, int n, float dt,
+                                                               uint16_t* cache, int n, float dt, int repeat,
                                                                double* __restrict__ stats) {
   const int64_t base = int64_t(blockIdx.x) * n;
   float* xr = x + base;
@@ -77,14 +83,14 @@ __global__ __launch_bounds__(kFlowThreads) void flow_step_rows(float* __restrict
           s.add(f[2 * e + 1], bf16_hi(cp[e]));
         }
       }
-      x0.x = euler(x0.x, dt, f[0]);
-      x0.y = euler(x0.y, dt, f[1]);
-      x0.z = euler(x0.z, dt, f[2]);
-      x0.w = euler(x0.w, dt, f[3]);
-      x1.x = euler(x1.x, dt, f[4]);
-      x1.y = euler(x1.y, dt, f[5]);
-      x1.z = euler(x1.z, dt, f[6]);
-      x1.w = euler(x1.w, dt, f[7]);
+      x0.x = euler(x0.x, dt, f[0], repeat);
+      x0.y = euler(x0.y, dt, f[1], repeat);
+      x0.z = euler(x0.z, dt, f[2], repeat);
+      x0.w = euler(x0.w, dt, f[3], repeat);
+      x1.x = euler(x1.x, dt, f[4], repeat);
+      x1.y = euler(x1.y, dt, f[5], repeat);
+      x1.z = euler(x1.z, dt, f[6], repeat);
+      x1.w = euler(x1.w, dt, f[7], repeat);
       *reinterpret_cast<float4*>(xr + i) = x0;
       *reinterpret_cast<float4*>(xr + i + 4) = x1;
       if constexpr (FRESH) *reinterpret_cast<uint4*>(cr + i) = vw;
@@ -94,7 +100,7 @@ __global__ __launch_bounds__(kFlowThreads) void flow_step_rows(float* __restrict
       const uint16_t vb = vr[i];
       const float f = __uint_as_float(uint32_t(vb) << 16);
       if constexpr (STATS) s.add(f, __uint_as_float(uint32_t(cr[i]) << 16));
-      xr[i] = euler(xr[i], dt, f);
+      xr[i] = euler(xr[i], dt, f, repeat);
       if constexpr (FRESH) cr[i] = vb;
     }
   }
@@ -119,24 +125,24 @@ __global__ __launch_bounds__(kFlowThreads) void flow_step_rows(float* __restrict
 }
 
 template <bool FRESH, bool STATS>
-hipError_t launch_rows(float* x, const uint16_t* v, uint16_t* cache, int B, int n, float dt, double* stats,
-                       hipStream_t stream) {
+hipError_t launch_rows(float* x, const uint16_t* v, uint16_t* cache, int B, int n, float dt, int repeat,
+                       double* stats, hipStream_t stream) {
   if (n % 8 == 0)
     hipLaunchKernelGGL((flow_step_rows<FRESH, STATS, true>), dim3(B), dim3(kFlowThreads), 0, stream, x, v, cache, n,
-                       dt, stats);
+                       dt, repeat, stats);
   else
     hipLaunchKernelGGL((flow_step_rows<FRESH, STATS, false>), dim3(B), dim3(kFlowThreads), 0, stream, x, v, cache, n,
-                       dt, stats);
+                       dt, repeat, stats);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_flow_step(float* x, const uint16_t* v, uint16_t* cache, int B, int n, float dt, double* stats,
-                            hipStream_t stream) {
-  if (!v) return launch_rows<false, false>(x, v, cache, B, n, dt, stats, stream);
-  if (!stats) return launch_rows<true, false>(x, v, cache, B, n, dt, stats, stream);
-  return launch_rows<true, true>(x, v, cache, B, n, dt, stats, stream);
+hipError_t launch_flow_step(float* x, const uint16_t* v, uint16_t* cache, int B, int n, float dt, int repeat,
+                            double* stats, hipStream_t stream) {
+  if (!v) return launch_rows<false, false>(x, v, cache, B, n, dt, repeat, stats, stream);
+  if (!stats) return launch_rows<true, false>(x, v, cache, B, n, dt, repeat, stats, stream);
+  return launch_rows<true, true>(x, v, cache, B, n, dt, repeat, stats, stream);
 }
 
 }  // namespace w4a8

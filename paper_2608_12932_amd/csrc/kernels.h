@@ -107,9 +107,11 @@ size_t stream_attention_workspace(int H, int Nq, int Nk);
 // ---- flow-matching Euler step with the velocity cache (flow.hip)
 // v == nullptr: a reused step (x += dt * cache); otherwise cache = v after
 // x += dt * v, and, with stats, stats[b] = (sum v c, sum v v, sum c c,
-// sum (v - c)^2) against the cache before the step.  One workgroup per row.
-hipError_t launch_flow_step(float* x, const uint16_t* v, uint16_t* cache, int B, int n, float dt, double* stats,
-                            hipStream_t stream);
+// sum (v - c)^2) against the cache before the step; the update is applied
+// `repeat` times (consecutive steps with the same velocity).  One workgroup
+// per row.
+hipError_t launch_flow_step(float* x, const uint16_t* v, uint16_t* cache, int B, int n, float dt, int repeat,
+                            double* stats, hipStream_t stream);
 
 const char* smallm_kernel_name(const SmallMPlan& p);
 const char* largem_kernel_name(const LargeMPlan& p);

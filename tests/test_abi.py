@@ -212,15 +212,17 @@ def test_flow_step_rejections():
     P = ctypes.c_void_p
     X, V, C, S = P(1 << 24), P(2 << 24), P(3 << 24), P(4 << 24)  # disjoint fake addresses
     f = L.w4a8_flow_step
-    assert f(X, None, C, 6, 128, 0.125, S, None) == w.W4A8_EINVAL      # stats on a reused step
-    assert f(X, V, C, 6, 0, 0.125, None, None) == w.W4A8_EINVAL        # n >= 1
-    assert f(X, V, C, -1, 8, 0.125, None, None) == w.W4A8_EINVAL
-    assert f(X, V, C, (1 << 24) + 1, 8, 0.125, None, None) == w.W4A8_EINVAL
-    assert f(X, V, C, 6, 128, float("inf"), None, None) == w.W4A8_EINVAL
-    assert f(X, V, C, 6, 128, float("nan"), None, None) == w.W4A8_EINVAL
-    assert f(P((1 << 24) + 4), V, C, 6, 128, 0.125, None, None) == w.W4A8_EINVAL   # misaligned x
-    assert f(X, V, C, 6, 128, 0.125, P((4 << 24) + 4), None) == w.W4A8_EINVAL      # misaligned stats
-    assert f(X, V, P((1 << 24) + 1024), 6, 128, 0.125, None, None) == w.W4A8_EINVAL  # cache inside x
-    assert f(X, P((3 << 24) + 16), C, 6, 128, 0.125, None, None) == w.W4A8_EINVAL   # v_new straddles the cache
-    assert f(X, V, C, 6, 128, 0.125, P((2 << 24) + 64), None) == w.W4A8_EINVAL      # stats inside v_new
-    assert f(None, None, None, 0, 128, 0.125, None, None) == w.W4A8_OK               # B == 0 is a no-op
+    assert f(X, None, C, 6, 128, 0.125, 1, S, None) == w.W4A8_EINVAL      # stats on a reused step
+    assert f(X, V, C, 6, 0, 0.125, 1, None, None) == w.W4A8_EINVAL        # n >= 1
+    assert f(X, V, C, -1, 8, 0.125, 1, None, None) == w.W4A8_EINVAL
+    assert f(X, V, C, (1 << 24) + 1, 8, 0.125, 1, None, None) == w.W4A8_EINVAL
+    assert f(X, V, C, 6, 128, float("inf"), 1, None, None) == w.W4A8_EINVAL
+    assert f(X, V, C, 6, 128, float("nan"), 1, None, None) == w.W4A8_EINVAL
+    assert f(P((1 << 24) + 4), V, C, 6, 128, 0.125, 1, None, None) == w.W4A8_EINVAL   # misaligned x
+    assert f(X, V, C, 6, 128, 0.125, 1, P((4 << 24) + 4), None) == w.W4A8_EINVAL      # misaligned stats
+    assert f(X, V, P((1 << 24) + 1024), 6, 128, 0.125, 1, None, None) == w.W4A8_EINVAL  # cache inside x
+    assert f(X, P((3 << 24) + 16), C, 6, 128, 0.125, 1, None, None) == w.W4A8_EINVAL   # v_new straddles the cache
+    assert f(X, V, C, 6, 128, 0.125, 1, P((2 << 24) + 64), None) == w.W4A8_EINVAL      # stats inside v_new
+    assert f(X, V, C, 6, 128, 0.125, 0, None, None) == w.W4A8_EINVAL                # repeat >= 1
+    assert f(X, V, C, 6, 128, 0.125, 4097, None, None) == w.W4A8_EINVAL
+    assert f(None, None, None, 0, 128, 0.125, 1, None, None) == w.W4A8_OK               # B == 0 is a no-op

@@ -93,6 +93,27 @@ def test_flow_step_full_size_sampled_rows():
     check_step(x0, v, c, 0.125, True, "full size", rows=rows)
 
 
+@pytest.mark.parametrize("B,n,seed", [(6, 128, 71), (3, 1000, 72), (257, 2048, 73)])
+@pytest.mark.parametrize("repeat", [2, 5])
+@pytest.mark.parametrize("fresh", [True, False])
+def test_flow_step_repeat_equals_separate_steps(B, n, seed, repeat, fresh):
+    print(f"[case] flow step repeat={repeat} fresh={fresh} B={B} n={n}", flush=True)
+    x0 = I.flow_state(B, n, seed)
+    c = I.flow_velocity(B, n, seed + 100)
+    v = I.flow_velocity(B, n, seed + 200) if fresh else None
+    x = torch.from_numpy(x0).to("cuda:0")
+    cd = dev_bf16(c)
+    st = w.w4a8_flow_step(x, None if v is None else dev_bf16(v), cd, 0.125, stats=fresh, repeat=repeat)
+    torch.cuda.synchronize()
+    xo, co, so = oracle.flow_step(x0, v, c, 0.125)
+    for _ in range(repeat - 1):
+        xo, co, _ = oracle.flow_step(xo, None, co, 0.125)
+    np.testing.assert_array_equal(x.cpu().numpy().view(np.uint32), xo.view(np.uint32))
+    np.testing.assert_array_equal(host_bits(cd), co)
+    if fresh:
+        assert (np.abs(st.cpu().numpy() - so) <= stat_bound(v, c)).all()
+
+
 def test_flow_step_empty_batch():
     c = torch.zeros((0, 8), dtype=torch.bfloat16, device="cuda:0")
     x = torch.zeros((0, 8), dtype=torch.float32, device="cuda:0")
@@ -104,6 +125,39 @@ def _velocity(x, t):
     function of the state and time, evaluated on the host for both sides."""
     return I.to_bf16_bits(np.tanh(0.5 * x).astype(np.float32) * np.float32(1.0 + 2.0 * (t - 0.5) ** 2)
                           + np.float32(t))
+
+
+def runs(fresh):
+    """(step, repeat) per evaluated step: the step and the reused steps after it."""
+    out = []
+    for i, f in enumerate(fresh):
+        if f:
+            out.append([i, 1])
+        else:
+            out[-1][1] += 1
+    return out
+
+
+@pytest.mark.parametrize("B,n,n_reuse", [(6, 128, 4), (33, 1000, 4), (8, 4096, 3), (6, 128, 7)])
+def test_flow_solve_fused_runs(B, n, n_reuse):
+    # one call per evaluated step, its reused steps folded in with repeat
+    print(f"[case] flow solve fused runs B={B} n={n} steps=8 reuse={n_reuse}", flush=True)
+    n_steps = 8
+    x0 = I.flow_state(B, n, 52)
+    xo, _, stats_o = oracle.flow_solve(x0, _velocity, n_steps, n_reuse)
+    x = torch.from_numpy(x0).to("cuda:0")
+    cache = torch.zeros((B, n), dtype=torch.bfloat16, device="cuda:0")
+    c_host = np.zeros((B, n), np.uint16)
+    dt = np.float32(1.0) / np.float32(n_steps)
+    rs = runs(w.w4a8_flow_schedule(n_steps, n_reuse))
+    assert len(rs) == n_steps - n_reuse and sum(r for _, r in rs) == n_steps
+    for k, (i, r) in enumerate(rs):
+        vb = _velocity(x.cpu().numpy(), i / n_steps)
+        st = w.w4a8_flow_step(x, dev_bf16(vb), cache, dt, stats=True, repeat=r).cpu().numpy()
+        assert (np.abs(st - stats_o[k]) <= stat_bound(vb, c_host)).all(), f"run {k}: stats"
+        c_host = vb
+    np.testing.assert_array_equal(x.cpu().numpy().view(np.uint32), xo.view(np.uint32))
+    np.testing.assert_array_equal(host_bits(cache), c_host)
 
 
 @pytest.mark.parametrize("B,n,n_reuse", [(6, 128, 4), (6, 128, 0), (33, 1000, 4), (8, 4096, 3)])

@@ -94,6 +94,40 @@ def test_queries_seeing_one_key_and_all_keys():
     check(2, 1, pos_q, pos_k, 803, "edge visibility")
 
 
+def test_cache_shorter_than_one_tile():
+    # 14 keys: one partial key tile; 7 queries: one partial query block
+    pos_k, pos_q = window(1, 2, 7, 1)
+    check(2, 2, pos_q, pos_k, 805, "window 1x2x7")
+
+
+def test_query_seeing_no_key_gets_zero():
+    pos_k = np.arange(10, 110, dtype=np.int32)
+    pos_q = np.array([5, 50, 3, 109], np.int32)
+    H, Hkv = 2, 1
+    q = I.activations(H * 4, D, 806).reshape(H, 4, D)
+    k = I.activations(Hkv * 100, D, 807).reshape(Hkv, 100, D)
+    v = I.activations(Hkv * 100, D, 808).reshape(Hkv, 100, D)
+    cos_t, sin_t = oracle.rope_tables(110, D, base=1e6)
+    o = run(q, k, v, pos_q, pos_k, cos_t, sin_t, 1.0 / np.sqrt(D))
+    assert (o[:, [0, 2]] == 0).all()
+    sel = np.array([1, 3])
+    o64, bnd = oracle.streaming_attention(q[:, sel], k, v, pos_q[sel], pos_k, cos_t, sin_t, np.float32(1.0 / np.sqrt(D)))
+    assert (np.abs(o[:, sel] - o64) <= 2.0 ** -8 * np.abs(o64) + 2.0 ** -8 * bnd + 1e-30).all()
+
+
+def test_long_cache_without_tile_skipping():
+    # 10 frames x 4096 tokens of one view (40960 keys) under 4096 queries: so
+    # many query blocks that the key range splits in 2 only, with more tiles
+    # per split than the skip table holds, so every tile is computed and
+    # masked (the path without tile skipping); 64 sampled queries
+    pos_k, pos_q = window(1, 10, 4096, 3)
+    H, Hkv, Nq, Nk = 8, 2, len(pos_q), len(pos_k)
+    S = w.w4a8_stream_attention_workspace_bytes(H, Nq, Nk) // (H * Nq * 130 * 4)
+    assert S >= 1 and (Nk // 32) / S > 512
+    rows = np.sort(np.random.Generator(np.random.PCG64(809)).choice(Nq, 64, replace=False))
+    check(H, Hkv, pos_q, pos_k, 810, "long cache 1x10x4096", rows=rows)
+
+
 def test_rejected_calls():
     L = w.lib()
     import ctypes

@@ -422,7 +422,7 @@ def bench_stream_attention(steps):
     ptrs = (q.data_ptr(), k.data_ptr(), v.data_ptr(), pq.data_ptr(), pk.data_ptr(), cos_t.data_ptr(), sin_t.data_ptr())
 
     need = int(L.w4a8_stream_attention_workspace_bytes(H, Nq, Nk))
-    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(max(need, 1), dtype=torch.uint8, device=dev)
 
     def call(i, stream):
         rc = L.w4a8_stream_attention(*ptrs, n_pos, H, Hkv, Nq, Nk, D, 1.0 / np.sqrt(D), o.data_ptr(),

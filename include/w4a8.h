@@ -177,7 +177,10 @@ w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, 
  *   workspace    device, >= w4a8_stream_attention_workspace_bytes(H, Nq, Nk)
  *                bytes, 256-byte aligned (may be NULL if that is 0): the
  *                partial results of key-range splits, written before read
- *                (no zero fill needed); concurrent calls must not share it
+ *                (no zero fill needed), past the first 64 KiB, which this
+ *                call leaves untouched, so that it may share one buffer
+ *                with w4a8_linear's workspace; concurrent calls must not
+ *                share it
  * A query that sees no key gets 0.  Does not synchronize; enqueues kernels
  * only.
  */
@@ -197,7 +200,9 @@ size_t w4a8_stream_attention_workspace_bytes(int64_t H, int64_t Nq, int64_t Nk);
  * The caller must
  * zero-fill a workspace once before its first use; every call leaves its
  * counters at zero again, so the same workspace can be reused by later
- * calls on the same stream.  Returns 0 as well for invalid shapes.
+ * calls on the same stream.  The counters of every shape sit in the first
+ * 64 KiB, which nothing else writes, so calls of different shapes (and
+ * w4a8_stream_attention) can share one workspace.  Returns 0 as well for invalid shapes.
  */
 size_t w4a8_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind);
 

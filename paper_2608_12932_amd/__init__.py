@@ -312,7 +312,7 @@ def w4a8_stream_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos
         wk_ptr, wk_bytes = None, 0
     else:
         if workspace is None:
-            workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+            workspace = torch.zeros(need, dtype=torch.uint8, device=q.device)
         buf = workspace.get(need) if isinstance(workspace, Workspace) else workspace
         wk_ptr, wk_bytes = _dev(buf, "workspace", torch.uint8), buf.numel()
     rc = lib().w4a8_stream_attention(_dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),

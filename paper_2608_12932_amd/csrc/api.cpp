@@ -31,24 +31,27 @@ struct Plan {
   LargeMPlan lm{};
   // workspace layout (bytes)
   size_t off_counters = 0, off_partial = 0, off_xq = 0, off_sx = 0, total = 0;
+  bool counters_fit = true;  // the split's counters fit the counter region
 };
 
 Plan make_plan(int64_t M, int64_t N, int64_t K, bool group, bool bf16_in, bool swiglu = false) {
   Plan p;
   p.small_m = M <= kSmallMMaxM;
-  size_t off = 0;
   if (p.small_m) {
     p.sm = plan_smallm((int)M, (int)N, (int)K, group, bf16_in, swiglu);
     p.separate_quant = bf16_in && !p.sm.fused;
-    if (p.sm.S > 1) {
-      p.off_counters = off;
-      off = round_up(off + (size_t)p.sm.groups * sizeof(unsigned), 256);
-      p.off_partial = off;
-      off = round_up(off + (size_t)p.sm.S * M * N * 4, 256);
-    }
   } else {
     p.lm = plan_largem((int)M, (int)N, (int)K, group, swiglu);
     p.separate_quant = bf16_in;
+  }
+  // counters at offset 0 of the shared counter region, the rest beyond it
+  const bool split = p.small_m && p.sm.S > 1;
+  p.counters_fit = !split || p.sm.groups <= kMaxCounters;
+  size_t off = split || p.separate_quant ? kCounterRegionBytes : 0;
+  if (split) {
+    p.off_counters = 0;
+    p.off_partial = off;
+    off = round_up(off + (size_t)p.sm.S * M * N * 4, 256);
   }
   if (p.separate_quant) {
     p.off_xq = off;
@@ -97,6 +100,7 @@ w4a8_status run_linear(const void* x, int in_kind, const float* x_scale, int64_t
   const bool group = scale_mode == W4A8_SCALE_GROUP_F16 && out_kind != W4A8_OUT_I32_ACC;
   const bool bf16_in = in_kind == W4A8_IN_BF16;
   const Plan p = make_plan(M, N, K, group, bf16_in, swiglu);
+  if (!p.counters_fit) return W4A8_EUNSUPPORTED;
   if (workspace_bytes < p.total) return W4A8_EINVAL;
   if (p.total && (!workspace || !aligned(workspace, 256))) return W4A8_EINVAL;
 

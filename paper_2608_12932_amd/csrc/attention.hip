@@ -350,10 +350,12 @@ int stream_attention_splits(int H, int Nq, int Nk) {
   return S;
 }
 
+// Workspace: the partials, past the counter region shared with the linear
+// calls' workspaces (left untouched here).
 size_t stream_attention_workspace(int H, int Nq, int Nk) {
   const int S = stream_attention_splits(H, Nq, Nk);
   if (S == 1) return 0;
-  return (size_t)S * H * Nq * (kD + 2) * sizeof(float);
+  return kCounterRegionBytes + (size_t)S * H * Nq * (kD + 2) * sizeof(float);
 }
 
 hipError_t launch_stream_attention(const AttnArgs& a0, hipStream_t stream) {
@@ -364,7 +366,7 @@ hipError_t launch_stream_attention(const AttnArgs& a0, hipStream_t stream) {
   a.tiles_per_split = (ntiles + a.S - 1) / a.S;
   a.S = (ntiles + a.tiles_per_split - 1) / a.tiles_per_split;  // no empty trailing split
   if (a.S > 1) {
-    a.part_o = static_cast<float*>(a.workspace);
+    a.part_o = reinterpret_cast<float*>(static_cast<uint8_t*>(a.workspace) + kCounterRegionBytes);
     a.part_ml = a.part_o + (size_t)a.S * a.H * a.Nq * kD;
   }
   const dim3 grid((unsigned)((a.Nq + kQPerBlock - 1) / kQPerBlock), (unsigned)a.H, (unsigned)a.S);

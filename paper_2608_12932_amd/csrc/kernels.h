@@ -9,6 +9,13 @@ namespace w4a8 {
 
 enum OutKind { kOutBF16 = 0, kOutF32 = 1, kOutI32 = 2 };
 
+// Every workspace starts with this region of arrival counters, at the same
+// offsets for every call shape, and everything else a call keeps there
+// (partial sums, codes) lies beyond it: counters return to zero at the end
+// of each call, so one zero-filled workspace serves calls of any shape.
+constexpr size_t kCounterRegionBytes = 64 * 1024;
+constexpr int kMaxCounters = (int)(kCounterRegionBytes / sizeof(unsigned));
+
 // ---- activation quantize (quantize.hip)
 hipError_t launch_quantize(const uint16_t* x, int M, int K, int8_t* q, float* scale,
                            hipStream_t stream);

@@ -187,7 +187,7 @@ def test_stream_attention_rejections():
     assert f(*args(Nq=0)) == w.W4A8_OK
     # a shape that splits its key range needs the workspace
     need = w.w4a8_stream_attention_workspace_bytes(32, 768, 3072)
-    assert need == 2 * 32 * 768 * (128 + 2) * 4
+    assert need == 64 * 1024 + 2 * 32 * 768 * (128 + 2) * 4  # counter region, then the partials
     assert f(*args(H=32, Hkv=8, Nq=768, Nk=3072)) == w.W4A8_EINVAL
     assert f(*args(H=32, Hkv=8, Nq=768, Nk=3072, ws=P((1 << 20) + 16), wsb=need)) == w.W4A8_EINVAL  # misaligned
     assert w.w4a8_stream_attention_workspace_bytes(4, 64, 256) == 0

@@ -1,0 +1,44 @@
+"""One zero-filled workspace shared by calls of different shapes: a K-split
+call (arrival counters), a call whose bf16 input is quantized into the
+workspace, a split streaming attention, then the K-split call again.  Every
+call's counters sit in the workspace's first 64 KiB, which nothing else
+writes, so the repeated call must still give the oracle's bits."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_12932_amd as w
+from paper_2608_12932_amd import inputs as I
+from helpers import dev, pack, run_linear
+
+pytestmark = pytest.mark.gpu
+
+
+def test_workspace_shared_across_shapes():
+    ws = w.Workspace(dev())
+    shapes = [(1, 16, 65536, 11), (16, 4096, 4096, 12)]
+    assert "S=8 " in w.w4a8_linear_describe(1, 16, 65536, 0, 0)
+    assert "quantize_rows" in w.w4a8_linear_describe(16, 4096, 4096, 0, 0)
+    cases = []
+    for M, N, K, seed in shapes:
+        x = I.activations(M, K, seed)
+        W, s = I.weights(N, K, seed + 1)
+        cases.append((x, pack(W), s, N, oracle.linear(x, W, s_w=s, nthreads=8)["y"]))
+    H, Nq, Nk = 2, 64, 2048
+    assert w.w4a8_stream_attention_workspace_bytes(H, Nq, Nk) > 64 * 1024
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev()).view(torch.bfloat16)
+    q = t(I.activations(H * Nq, 128, 20).reshape(H, Nq, 128))
+    k = t(I.activations(H * Nk, 128, 21).reshape(H, Nk, 128))
+    v = t(I.activations(H * Nk, 128, 22).reshape(H, Nk, 128))
+    cos_t, sin_t = (torch.from_numpy(a).to(dev()) for a in oracle.rope_tables(Nk, 128))
+    pq = torch.arange(Nk - Nq, Nk, dtype=torch.int32, device=dev())
+    pk = torch.arange(Nk, dtype=torch.int32, device=dev())
+    for order in ([0, 1, 0], [1, 0, 1, 0]):
+        for i in order:
+            x, wp, s, N, want = cases[i]
+            print(f"[case] shared workspace shape {shapes[i][:3]}", flush=True)
+            got = run_linear(x, wp, s, N, group=False, out_kind=w.OUT_BF16, workspace=ws)
+            np.testing.assert_array_equal(got, want, err_msg=f"shape {shapes[i][:3]}")
+            w.w4a8_stream_attention(q, k, v, pq, pk, cos_t, sin_t, 128 ** -0.5, workspace=ws)
+            torch.cuda.synchronize()

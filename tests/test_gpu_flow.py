@@ -57,7 +57,7 @@ def check_step(x0, v_bits, c_bits, dt, stats, label, rows=None):
 # the paper's shape (6 samples x 64 waypoints x 2), the 16-byte path with
 # one, several and a ragged last pass, the one-element path on ragged rows
 SHAPES = [(6, 128, 1), (1, 1, 2), (1, 3, 3), (3, 1000, 4), (5, 8, 5), (4, 2056, 6), (2, 4104, 7), (257, 2048, 8),
-          (7, 16383, 9), (64, 16384, 10)]
+          (7, 16383, 9), (64, 16384, 10), (1000, 129, 11), (16384, 8, 12)]
 
 
 @pytest.mark.parametrize("B,n,seed", SHAPES)

@@ -612,6 +612,54 @@ def bench_stack(steps, layers=36):
                         "group-128 fp16 scales)", "rows": rows}
 
 
+def profile_workload(spec: str, steps: int, warmup: int):
+    """One workload alone, for a rocprofv3 run: `steps` timed steps after
+    `warmup`, each step as in the JSON line (bf16 x in, bf16 y out).  spec:
+      gate_up        gate+up verify step, M=16 (and the GEMM on int8 codes)
+      qkv            qkv prefill step, M=1024 (and the GEMM on int8 codes)
+      down:M         down verify, K=12288 N=4096, M in 1, 4, 16
+      layer:M        one decoder layer with group-128 scales, M in 1, 16, 256, 2048
+    Prints one JSON object with the event-timed us per step."""
+    import torch
+    import paper_2608_12932_amd as w
+    from paper_2608_12932_amd import inputs as I
+
+    name, _, arg = spec.partition(":")
+    if name == "gate_up":
+        d, ms, nbytes, ms_gemm, gemm_bytes = bench_gate_up(steps, warmup)
+        return {"profile": spec, "us_step": round(ms * 1e3, 3), "us_gemm": round(ms_gemm * 1e3, 3),
+                "step_bytes": nbytes, "gemm_bytes": gemm_bytes, "kernel": w.w4a8_linear_describe(16, d["N"], d["K"])}
+    if name == "qkv":
+        r = bench_qkv(steps, warmup)
+        return {"profile": spec, "us_step": round(r["ms_step"] * 1e3, 3), "us_gemm": round(r["ms_gemm"] * 1e3, 3),
+                "ops": r["ops"], "kernel": w.w4a8_linear_describe(r["M"], r["N"], r["K"])}
+    M = int(arg)
+    cache = {}
+    if name == "down":
+        xd, wps, sd, y, K, N, sbytes = _dev_inputs("down_verify", M, 0, 16, cache)
+        calls = [DirectCall(xd, wps, sd, N, y, workspace=w.Workspace(xd.device))]
+        nbytes = N * K // 2 + sbytes + M * K * 2 + M * N * 2
+        kinds = [w.w4a8_linear_describe(M, N, K)]
+    elif name == "layer":
+        calls, nbytes, kinds = [], 0, []
+        for mi, (mname, K, N) in enumerate(I.LAYER_MATS):
+            xd, wps, sd, y, K, N, sbytes = _dev_inputs("layer_group", M, mi, 6, cache)
+            calls.append(DirectCall(xd, wps, sd, N, y, workspace=w.Workspace(xd.device), scale_mode=w.SCALE_GROUP_F16))
+            nbytes += N * K // 2 + sbytes + M * K * 2 + M * N * 2
+            kinds.append(f"{mname}: " + w.w4a8_linear_describe(M, N, K, w.SCALE_GROUP_F16))
+    else:
+        raise SystemExit(f"unknown profile workload {spec!r}")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def step(i):
+        for c in calls:
+            c(i, stream)
+
+    ms = time_steps(step, steps, warmup)
+    return {"profile": spec, "us_step": round(ms * 1e3, 3), "algorithmic_bytes": nbytes,
+            "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1), "kernels": kinds}
+
+
 def measure_ceilings():
     """Measured HBM-read and INT8-MFMA ceilings (libw4a8_ceiling.so): a plain
     16-byte streaming read of 1 GiB, and independent 32x32x32 int8 MFMA
@@ -653,23 +701,53 @@ def measure_ceilings():
                           "what": "4 independent v_mfma_i32_32x32x32_i8 chains per wave, 4096 waves"}}
 
 
-def cpu_baseline(d, algo_bytes, budget_s=10.0):
-    """The oracle on the full gate+up verify layer, repeated until about
-    budget_s seconds of CPU work have run; the rate is the median run's."""
+def host_cpu():
+    """The host's logical CPU count, the CPUs this process may run on, and
+    the CPU model name (from /proc/cpuinfo, as lscpu reports it)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)), "model": model}
+
+
+def cpu_baseline(d, algo_bytes, budget_s=10.0, budget_1t_s=8.0):
+    """The oracle on the full gate+up verify layer: with one thread per token
+    row (the oracle splits the rows over threads, so at most M = 16), up to
+    the CPUs this process may use, repeated for about budget_s seconds of
+    CPU work; and on one thread for about budget_1t_s.  The rates are the
+    median run's.  The oracle is plain scalar C (int64 dot products), a
+    correctness reference, not a tuned CPU GEMM."""
     import oracle
 
-    threads = min(d["M"], len(os.sched_getaffinity(0)))
-    times = []
-    t_start = time.perf_counter()
-    while not times or (time.perf_counter() - t_start < budget_s and len(times) < 1000):
-        t0 = time.perf_counter()
-        oracle.linear(d["x"], d["W"], s_w=d["s"], nthreads=threads)
-        times.append(time.perf_counter() - t0)
-    t = statistics.median(times)
+    cpu = host_cpu()
+
+    def timed(threads, budget):
+        times = []
+        t_start = time.perf_counter()
+        while not times or (time.perf_counter() - t_start < budget and len(times) < 1000):
+            t0 = time.perf_counter()
+            oracle.linear(d["x"], d["W"], s_w=d["s"], nthreads=threads)
+            times.append(time.perf_counter() - t0)
+        return statistics.median(times), times
+
+    threads = min(d["M"], cpu["affinity"])
+    t, times = timed(threads, budget_s)
+    t1, times1 = timed(1, budget_1t_s)
     return {"value": round(algo_bytes / t / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "host": cpu,
+            "one_thread": {"value": round(algo_bytes / t1 / 1e9, 4), "unit": "GB/s", "ms_per_run": round(t1 * 1e3, 1),
+                           "runs": len(times1)},
             "sample": f"the full gate+up verify layer (M=16 K=4096 N=24576: quantize, int64 contraction, "
-                      f"dequant) run {len(times)} times ({sum(times):.1f} s of CPU work on {threads} threads), "
-                      f"median {t*1e3:.1f} ms per run"}
+                      f"dequant) run {len(times)} times on {threads} threads ({sum(times):.1f} s), median "
+                      f"{t*1e3:.1f} ms per run; and {len(times1)} times on 1 thread ({sum(times1):.1f} s), median "
+                      f"{t1*1e3:.1f} ms; host {cpu['model']}, {cpu['nproc']} logical CPUs, {cpu['affinity']} "
+                      f"available to this process"}
 
 
 def main():
@@ -687,6 +765,8 @@ def main():
                     help="run only the streaming attention workload (for profiling its kernels)")
     ap.add_argument("--flow-only", action="store_true",
                     help="run only the flow-matching step workloads (for profiling their kernel)")
+    ap.add_argument("--profile", default=None, metavar="WORKLOAD",
+                    help="run one workload only, for rocprofv3: gate_up, qkv, down:M, layer:M")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
@@ -698,6 +778,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     w.lib()
+    if args.profile:
+        print(json.dumps(profile_workload(args.profile, args.steps, args.warmup)), flush=True)
+        return
     if args.attention_only:
         print(json.dumps(bench_stream_attention(max(50, args.steps // 4))), flush=True)
         return

@@ -35,6 +35,14 @@
  *   - Arguments are validated before anything is launched; an invalid call
  *     returns an error code and has no effect.  No call prints or aborts.
  *   - A HIP launch failure is reported as W4A8_EHIP.
+ *
+ * Shape of the interface, where it could have been drawn otherwise:
+ *   - the group size is not an argument: W4A8_SCALE_GROUP_F16 fixes it at
+ *     W4A8_GROUP_SIZE (128), the one group size the method uses here;
+ *   - the workspace size queries take the input kind, because only a bf16
+ *     input quantized by a separate kernel keeps codes in the workspace;
+ *   - N need only be a multiple of 16, the output channels of one packed
+ *     weight block, and K a multiple of 128, the k of one block.
  */
 #ifndef W4A8_H_
 #define W4A8_H_
@@ -146,14 +154,15 @@ w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, 
                                       int8_t* x_q, float* x_scale, hipStream_t stream);
 
 /*
- * Streaming prefill attention with pre-RoPE cached keys.  FlashDrive, Sec.
- * 3.1 ("Streaming design"): streaming inference encodes only the newest
- * frame, inserts its tokens at the last-frame slot of each camera view
- * (view-major layout) and keeps the KV cache of the earlier frames; keys are
- * cached before their rotary embedding and rotated at their current,
- * shifted window positions, and a streaming mask keeps cross-view causality
- * with only the newest frame's tokens as queries.  This call computes, for
- * every query head h and query i,
+ * Streaming prefill attention with pre-RoPE cached keys (FlashDrive, Sec.
+ * 3.1 and Fig. 3).  As the window of camera frames advances, the arriving
+ * frame's tokens take the last frame position of each view, in a cache
+ * ordered view by view, and are the only rows whose attention is computed;
+ * the keys and values of the older frames are reused from the cache.  Keys
+ * sit in the cache without their rotary embedding and are rotated at the
+ * positions they hold in the window now, and the mask lets a query see the
+ * keys at or before its own window position, which keeps causality across
+ * views.  This call computes, for every query head h and query i,
  *     o[h][i] = sum_j softmax_j(scale * RoPE(q[h][i], pos_q[i]) . RoPE(k[h'][j], pos_k[j])) v[h'][j]
  * over the keys j with pos_k[j] <= pos_q[i] (the causal order of the
  * window), h' = h / (H / Hkv) (grouped-query heads).

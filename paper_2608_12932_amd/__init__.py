@@ -9,6 +9,7 @@ loading fails loudly when the library has not been built.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
@@ -89,9 +90,19 @@ def status_string(status: int) -> str:
     return lib().w4a8_status_string(int(status)).decode()
 
 
+def _torch_stream(stream=None, device=None) -> torch.cuda.Stream:
+    return torch.cuda.current_stream(device) if stream is None else stream
+
+
 def _stream(stream=None) -> int:
-    s = torch.cuda.current_stream() if stream is None else stream
-    return s.cuda_stream
+    return _torch_stream(stream).cuda_stream
+
+
+def _alloc_on(stream):
+    """Context for allocating a call's outputs: on the call's stream when it
+    is not torch's current one, so that the caching allocator orders their
+    reuse after the call's kernels."""
+    return contextlib.nullcontext() if stream is None else torch.cuda.stream(stream)
 
 
 def _dev(t: torch.Tensor, name: str, dtype: torch.dtype) -> int:
@@ -120,7 +131,8 @@ def w4a8_pack_weights(w: torch.Tensor, out: torch.Tensor | None = None, stream=N
     if nbytes == 0:
         raise W4A8Error(W4A8_EINVAL, f"w4a8_pack_weights: shape {N}x{K}")
     if out is None:
-        out = torch.empty(nbytes, dtype=torch.uint8, device=w.device)
+        with _alloc_on(stream):
+            out = torch.empty(nbytes, dtype=torch.uint8, device=w.device)
     elif out.numel() != nbytes:
         raise ValueError(f"out must hold {nbytes} bytes")
     rc = lib().w4a8_pack_weights(_dev(w, "w", torch.int8), N, K, _dev(out, "out", torch.uint8),
@@ -132,8 +144,9 @@ def w4a8_pack_weights(w: torch.Tensor, out: torch.Tensor | None = None, stream=N
 def w4a8_quantize_act(x: torch.Tensor, stream=None):
     """x: bf16 [M][K] device tensor -> (codes int8 [M][K], scales fp32 [M])."""
     M, K = x.shape
-    q = torch.empty((M, K), dtype=torch.int8, device=x.device)
-    s = torch.empty((M,), dtype=torch.float32, device=x.device)
+    with _alloc_on(stream):
+        q = torch.empty((M, K), dtype=torch.int8, device=x.device)
+        s = torch.empty((M,), dtype=torch.float32, device=x.device)
     rc = lib().w4a8_quantize_act(_dev(x, "x", torch.bfloat16), M, K, _dev(q, "q", torch.int8),
                                  _dev(s, "s", torch.float32), _stream(stream))
     _check(rc, "w4a8_quantize_act")
@@ -149,8 +162,9 @@ def w4a8_rmsnorm_quantize_act(x: torch.Tensor, gamma: torch.Tensor, eps: float, 
     g_ptr = _dev(gamma, "gamma", torch.bfloat16)
     if tuple(gamma.shape) != (K,):
         raise ValueError(f"gamma must be [{K}]")
-    q = torch.empty((M, K), dtype=torch.int8, device=x.device)
-    s = torch.empty((M,), dtype=torch.float32, device=x.device)
+    with _alloc_on(stream):
+        q = torch.empty((M, K), dtype=torch.int8, device=x.device)
+        s = torch.empty((M,), dtype=torch.float32, device=x.device)
     rc = lib().w4a8_rmsnorm_quantize_act(x_ptr, g_ptr, float(eps), M, K, q.data_ptr(), s.data_ptr(), _stream(stream))
     _check(rc, "w4a8_rmsnorm_quantize_act")
     return q, s
@@ -181,7 +195,8 @@ def w4a8_flow_step(x: torch.Tensor, v_new, v_cache: torch.Tensor, dt: float, sta
     for name, t in (("v_cache", v_cache), ("v_new", v_new)):
         if t is not None and tuple(t.shape) != (B, n):
             raise ValueError(f"{name} must be [{B}][{n}]")
-    st = torch.empty((B, 4), dtype=torch.float64, device=x.device) if stats else None
+    with _alloc_on(stream):
+        st = torch.empty((B, 4), dtype=torch.float64, device=x.device) if stats else None
     rc = lib().w4a8_flow_step(x_ptr, v_ptr, c_ptr, B, n, float(dt), int(repeat),
                               None if st is None else st.data_ptr(), _stream(stream))
     _check(rc, "w4a8_flow_step")
@@ -199,17 +214,48 @@ def w4a8_linear_describe(M: int, N: int, K: int, scale_mode: int = SCALE_CHANNEL
 
 
 class Workspace:
-    """A zero-filled device buffer reused across w4a8_linear calls on one
-    stream (the calls leave its counters at zero).  Grows on demand."""
+    """A zero-filled device buffer reused across w4a8_linear calls (the calls
+    leave its counters at zero).  Grows on demand.  Calls that share one
+    Workspace must not overlap: use it from one stream at a time.
+
+    get(nbytes, stream) returns the buffer ordered for work on `stream`: a
+    grown buffer is allocated and zero-filled on that stream, and the
+    caching allocator keeps every buffer (also a replaced one) from reuse
+    until the work already queued on the streams that used it is done."""
 
     def __init__(self, device="cuda"):
         self.device = torch.device(device)
         self.buf = torch.zeros(0, dtype=torch.uint8, device=self.device)
 
-    def get(self, nbytes: int) -> torch.Tensor:
+    def get(self, nbytes: int, stream: torch.cuda.Stream | None = None) -> torch.Tensor:
+        s = _torch_stream(stream, self.device)
         if nbytes > self.buf.numel():
-            self.buf = torch.zeros(max(nbytes, 2 * self.buf.numel()), dtype=torch.uint8, device=self.device)
+            old = self.buf
+            with torch.cuda.stream(s):
+                self.buf = torch.zeros(max(nbytes, 2 * old.numel()), dtype=torch.uint8, device=self.device)
+            if old.numel():
+                old.record_stream(s)
+        elif self.buf.numel():
+            self.buf.record_stream(s)
         return self.buf
+
+
+def _workspace_ptr(workspace, need: int, device, stream):
+    """(pointer, bytes) of a workspace of at least `need` bytes for a call on
+    `stream`: a Workspace, a caller's uint8 tensor, or None for a temporary
+    buffer zero-filled on that stream (and released to the allocator on it,
+    so later work on the stream cannot see it reused early)."""
+    if need == 0:
+        return None, 0
+    s = _torch_stream(stream, device)
+    if workspace is None:
+        with torch.cuda.stream(s):
+            buf = torch.zeros(need, dtype=torch.uint8, device=device)
+    elif isinstance(workspace, Workspace):
+        buf = workspace.get(need, s)
+    else:
+        buf = workspace
+    return _dev(buf, "workspace", torch.uint8), buf.numel()
 
 
 def _linear_call(entry: str, x, w_packed, w_scale, N, out_cols, x_scale, scale_mode, out_kind, out,
@@ -232,18 +278,13 @@ def _linear_call(entry: str, x, w_packed, w_scale, N, out_cols, x_scale, scale_m
     else:
         ws_ptr = _dev(w_scale, "w_scale", torch.float32 if scale_mode == SCALE_CHANNEL_F32 else torch.float16)
     if out is None:
-        out = torch.empty((M, out_cols), dtype=_OUT_DTYPE[out_kind], device=x.device)
+        with _alloc_on(stream):
+            out = torch.empty((M, out_cols), dtype=_OUT_DTYPE[out_kind], device=x.device)
     elif tuple(out.shape) != (M, out_cols):
         raise ValueError(f"out must be [{M}][{out_cols}]")
     y_ptr = _dev(out, "out", _OUT_DTYPE[out_kind])
     need = int(getattr(lib(), entry + "_workspace_bytes")(M, N, K, scale_mode, in_kind))
-    if need == 0:
-        wk_ptr, wk_bytes = None, 0
-    else:
-        if workspace is None:
-            workspace = torch.zeros(need, dtype=torch.uint8, device=x.device)
-        buf = workspace.get(need) if isinstance(workspace, Workspace) else workspace
-        wk_ptr, wk_bytes = _dev(buf, "workspace", torch.uint8), buf.numel()
+    wk_ptr, wk_bytes = _workspace_ptr(workspace, need, x.device, stream)
     rc = getattr(lib(), entry)(x_ptr, in_kind, xs_ptr, M, K, wp_ptr, ws_ptr, scale_mode, N, y_ptr,
                                out_kind, wk_ptr, wk_bytes, _stream(stream))
     _check(rc, entry)
@@ -304,17 +345,12 @@ def w4a8_stream_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos
     if rope_cos.shape != rope_sin.shape or rope_cos.dim() != 2 or rope_cos.shape[1] != D // 2:
         raise ValueError("rotary tables must be [n_pos][D/2]")
     if out is None:
-        out = torch.empty((H, Nq, D), dtype=torch.bfloat16, device=q.device)
+        with _alloc_on(stream):
+            out = torch.empty((H, Nq, D), dtype=torch.bfloat16, device=q.device)
     elif tuple(out.shape) != (H, Nq, D):
         raise ValueError(f"out must be [{H}][{Nq}][{D}]")
     need = int(lib().w4a8_stream_attention_workspace_bytes(H, Nq, Nk)) if Nq else 0
-    if need == 0:
-        wk_ptr, wk_bytes = None, 0
-    else:
-        if workspace is None:
-            workspace = torch.zeros(need, dtype=torch.uint8, device=q.device)
-        buf = workspace.get(need) if isinstance(workspace, Workspace) else workspace
-        wk_ptr, wk_bytes = _dev(buf, "workspace", torch.uint8), buf.numel()
+    wk_ptr, wk_bytes = _workspace_ptr(workspace, need, q.device, stream)
     rc = lib().w4a8_stream_attention(_dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
                                      _dev(v, "v", torch.bfloat16), _dev(pos_q, "pos_q", torch.int32),
                                      _dev(pos_k, "pos_k", torch.int32), _dev(rope_cos, "rope_cos", torch.float32),

@@ -32,6 +32,7 @@ struct Plan {
   // workspace layout (bytes)
   size_t off_counters = 0, off_partial = 0, off_xq = 0, off_sx = 0, total = 0;
   bool counters_fit = true;  // the split's counters fit the counter region
+  bool grid_fits = true;     // the large-M tile count fits one launch
 };
 
 Plan make_plan(int64_t M, int64_t N, int64_t K, bool group, bool bf16_in, bool swiglu = false) {
@@ -43,6 +44,7 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, bool group, bool bf16_in, bool s
   } else {
     p.lm = plan_largem((int)M, (int)N, (int)K, group, swiglu);
     p.separate_quant = bf16_in;
+    p.grid_fits = p.lm.tiles >= 1 && p.lm.tiles <= kMaxGrid;
   }
   // counters at offset 0 of the shared counter region, the rest beyond it
   const bool split = p.small_m && p.sm.S > 1;
@@ -100,7 +102,7 @@ w4a8_status run_linear(const void* x, int in_kind, const float* x_scale, int64_t
   const bool group = scale_mode == W4A8_SCALE_GROUP_F16 && out_kind != W4A8_OUT_I32_ACC;
   const bool bf16_in = in_kind == W4A8_IN_BF16;
   const Plan p = make_plan(M, N, K, group, bf16_in, swiglu);
-  if (!p.counters_fit) return W4A8_EUNSUPPORTED;
+  if (!p.counters_fit || !p.grid_fits) return W4A8_EUNSUPPORTED;
   if (workspace_bytes < p.total) return W4A8_EINVAL;
   if (p.total && (!workspace || !aligned(workspace, 256))) return W4A8_EINVAL;
 
@@ -150,7 +152,7 @@ w4a8_status run_linear(const void* x, int in_kind, const float* x_scale, int64_t
     a.out_kind = out_kind;
     a.tiles_m = p.lm.tiles_m;
     a.tiles_n = p.lm.tiles_n;
-    a.xcd_remap = (p.lm.tiles_m * p.lm.tiles_n) % 8 == 0;
+    a.xcd_remap = p.lm.tiles % 8 == 0;
     a.F = swiglu ? (int)(N / 2) : 0;
     e = launch_largem(p.lm, a, stream);
   }
@@ -161,7 +163,8 @@ size_t workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_k
   if (M < 0 || M > W4A8_M_MAX || !valid_nk(N, K) || !valid_modes(scale_mode, in_kind)) return 0;
   if (M == 0 || (uint64_t)N * (uint64_t)K >= (uint64_t(1) << 37)) return 0;
   if (swiglu && !gated_shape(N)) return 0;
-  return make_plan(M, N, K, scale_mode == W4A8_SCALE_GROUP_F16, in_kind == W4A8_IN_BF16, swiglu).total;
+  const Plan p = make_plan(M, N, K, scale_mode == W4A8_SCALE_GROUP_F16, in_kind == W4A8_IN_BF16, swiglu);
+  return p.counters_fit && p.grid_fits ? p.total : 0;
 }
 
 const char* describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind, int out_kind, bool swiglu) {
@@ -170,6 +173,7 @@ const char* describe(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kin
   if (swiglu && !gated_shape(N)) return "invalid shape";
   const bool group = scale_mode == W4A8_SCALE_GROUP_F16 && out_kind != W4A8_OUT_I32_ACC;
   const Plan p = make_plan(M, N, K, group, in_kind == W4A8_IN_BF16, swiglu);
+  if (!p.counters_fit || !p.grid_fits) return "unsupported shape";
   snprintf(buf, sizeof buf, "%s%s workspace=%zu", p.separate_quant ? "quantize_rows + " : "",
            p.small_m ? smallm_kernel_name(p.sm) : largem_kernel_name(p.lm), p.total);
   return buf;

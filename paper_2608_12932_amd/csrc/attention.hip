@@ -1,12 +1,14 @@
-// Streaming prefill attention (FlashDrive Sec. 3.1, streaming design).
+// Streaming prefill attention (FlashDrive Sec. 3.1 and Fig. 3).
 //
-// Streaming inference encodes only the newest frame: its tokens are the
-// queries, the window's KV cache (the cached frames plus the new one, laid
-// out view-major) holds the keys and values.  Keys are cached before their
-// rotary embedding and rotated here at their current window positions, so
-// a slide of the window only changes the positions; the streaming mask
-// admits key j to query i iff pos_k[j] <= pos_q[i], the causal order of the
-// view-major window.
+// When the camera window advances by one frame, only the tokens of the
+// frame that just arrived need fresh attention rows: they form the query
+// set here, while the keys and values come from the whole window's cache
+// (older frames kept from earlier steps plus the arrival, ordered view by
+// view).  The cache stores keys without their rotary embedding; this
+// kernel rotates each key at the position it occupies in the window now,
+// so sliding the window changes only the position array.  Key j may be
+// seen by query i exactly when pos_k[j] <= pos_q[i], i.e. causally in the
+// view-major order of the window.
 //
 // One workgroup per (64 queries, head); each of its 4 waves owns 16
 // queries.  Key tiles that none of its queries can see are skipped.  Per

@@ -138,9 +138,10 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 //   s = a / 127 and inv = 1 / s are IEEE fp32 divisions.  Codes are
 //   round_half_even(fl(x / s)); for a >= 2^-96 fl(x / s) is obtained as
 //   p = x * inv corrected by one Markstein step (two fmas), which an
-//   exhaustive check over every pair of bf16 values (x, a) with |x| <= a
-//   shows to be the correctly rounded quotient; below 2^-96 the residual can
-//   underflow, so those rows use the IEEE division directly.
+//   exhaustive check over every pair of bf16 values (x, a) with |x| <= a and
+//   a >= 2^-96 (tests/quant_exhaustive.c, run by tests/test_quant_proof.py)
+//   shows to give the code of the correctly rounded quotient; below 2^-96
+//   the residual can underflow, so those rows use the IEEE division directly.
 struct QScale {
   float s, inv;
   int mode;  // 0: all-zero row, 1: reciprocal + correction, 2: IEEE division

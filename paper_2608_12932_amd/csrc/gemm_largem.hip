@@ -41,8 +41,8 @@ LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu) {
     if (swiglu ? !t.gated_ok : !t.plain_ok) continue;
     const int BM = 32 * t.WM * t.GM, BN = 32 * t.WN * t.GN;
     const int tm = (M + BM - 1) / BM, tn = swiglu ? (N / 2 + BN / 2 - 1) / (BN / 2) : (N + BN - 1) / BN;
-    const long tiles = (long)tm * tn;
-    const long rounds = (tiles + 255) / 256;
+    const int64_t tiles = (int64_t)tm * tn;
+    const int64_t rounds = (tiles + 255) / 256;
     const double eff = (double)M * N / ((double)rounds * 256.0 * BM * BN);
     const double score = eff * t.quality;
     if (score > best + 1e-9) {
@@ -53,6 +53,7 @@ LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu) {
       p.threads = 64 * t.GM * t.GN;
       p.tiles_m = tm;
       p.tiles_n = tn;
+      p.tiles = tiles;
     }
   }
   p.lds_bytes = (size_t)kMenu[p.cfg].ring * ((size_t)p.BM * 128 + (size_t)p.BN / 16 * kBlockBytes +
@@ -62,8 +63,8 @@ LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu) {
 
 hipError_t launch_largem(const LargeMPlan& p, const LargeMArgs& a, hipStream_t stream) {
   LargeMKernelFn k = p.group ? largem_group_kernel(p.cfg, p.swiglu) : channel_kernel(p.cfg, p.swiglu);
-  if (!k) return hipErrorInvalidValue;
-  const unsigned grid = (unsigned)(p.tiles_m * p.tiles_n);
+  if (!k || p.tiles < 1 || p.tiles > kMaxGrid) return hipErrorInvalidValue;
+  const unsigned grid = (unsigned)p.tiles;
   hipLaunchKernelGGL(k, dim3(grid), dim3(p.threads), p.lds_bytes, stream, a);
   return hipGetLastError();
 }

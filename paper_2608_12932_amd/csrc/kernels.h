@@ -79,8 +79,11 @@ struct LargeMPlan {
   bool group;
   bool swiglu;           // gated output (the 128 x 128 tile; a tile covers BN / 2 output columns)
   int tiles_m, tiles_n;
+  int64_t tiles;         // tiles_m * tiles_n, the grid size
   size_t lds_bytes;
 };
+// Largest grid a launch takes (one workgroup per tile).
+constexpr int64_t kMaxGrid = 0x7FFFFFFF;
 LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu);
 hipError_t launch_largem(const LargeMPlan& p, const LargeMArgs& a, hipStream_t stream);
 typedef void (*LargeMKernelFn)(const LargeMArgs);

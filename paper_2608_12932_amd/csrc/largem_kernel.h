@@ -90,7 +90,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   extern __shared__ __align__(16) uint8_t lds[];
 
   int bid = blockIdx.x;
-  const int total = a.tiles_m * a.tiles_n;
+  const int total = (int)gridDim.x;  // tiles_m * tiles_n (the host keeps it below 2^31)
   if (a.xcd_remap) bid = (bid & 7) * (total >> 3) + (bid >> 3);
   const int tm = bid % a.tiles_m, tn = bid / a.tiles_m;
   // Gated tiles: tile columns [0, BN/2) are gate columns f0 .., [BN/2, BN)

@@ -226,3 +226,16 @@ def test_flow_step_rejections():
     assert f(X, V, C, 6, 128, 0.125, 0, None, None) == w.W4A8_EINVAL                # repeat >= 1
     assert f(X, V, C, 6, 128, 0.125, 4097, None, None) == w.W4A8_EINVAL
     assert f(None, None, None, 0, 128, 0.125, 1, None, None) == w.W4A8_OK               # B == 0 is a no-op
+
+
+@pytest.mark.parametrize("scale_mode", [w.SCALE_CHANNEL_F32, w.SCALE_GROUP_F16])
+def test_largest_shapes_plan_a_grid_that_fits_one_launch(scale_mode):
+    # M = 2^20 rows over N = 2^24 columns: the tile count is formed in 64
+    # bits and the planned grid stays below 2^31 workgroups
+    M, N, K = 1 << 20, 1 << 24, 128
+    d = w.w4a8_linear_describe(M, N, K, scale_mode)
+    m = re.search(r"tiles=(\d+)x(\d+)", d)
+    assert m, d
+    assert int(m.group(1)) * int(m.group(2)) < 2 ** 31
+    assert w.w4a8_linear_workspace_bytes(M, N, K, scale_mode) >= M * K
+

@@ -240,6 +240,32 @@ w4a8_status w4a8_linear(const void* x, int in_kind, const float* x_scale, int64_
                         hipStream_t stream);
 
 /*
+ * w4a8_linear for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  It
+ * takes no workspace: the memory a call of w4a8_linear keeps in the caller's
+ * workspace (split-K partial sums and arrival counters, the codes and scales
+ * of a bf16 input quantized by a separate kernel) lives instead in a
+ * library-owned device array of W4A8_NOALLOC_SCRATCH_BYTES per GPU, held from
+ * the first call on a GPU until the process ends.  Arguments and results are
+ * those of w4a8_linear (the same kernels, the same bits).
+ *   - A problem whose w4a8_linear_workspace_bytes exceeds
+ *     W4A8_NOALLOC_SCRATCH_BYTES returns W4A8_EUNSUPPORTED before anything
+ *     is enqueued.
+ *   - No call allocates or frees memory or sets memory with a memset; a split
+ *     call clears its arrival counters with a small kernel, so the array
+ *     needs no initial contents.
+ *   - Every call on a GPU shares that GPU's array and finds the previous
+ *     call's contents there: calls on one stream are ordered, but calls that
+ *     can overlap on one GPU (different streams, or graphs replayed
+ *     concurrently) race and must not be issued.
+ *   - `stream` must belong to the current device.
+ */
+#define W4A8_NOALLOC_SCRATCH_BYTES (32u << 20)
+w4a8_status w4a8_linear_noalloc(const void* x, int in_kind, const float* x_scale, int64_t M, int64_t K,
+                                const uint8_t* w_packed, const void* w_scale, int scale_mode, int64_t N,
+                                void* y, int out_kind, hipStream_t stream);
+
+/*
  * Introspection for benchmarks and tests: a static, thread-local text
  * naming the kernels and tiling w4a8_linear would use for this problem and
  * its workspace size ("invalid shape" for a shape w4a8_linear rejects).

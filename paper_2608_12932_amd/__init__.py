@@ -28,7 +28,9 @@ EXPORTS = ("w4a8_status_string", "w4a8_packed_weight_bytes", "w4a8_pack_weights"
            "w4a8_quantize_act", "w4a8_linear_workspace_bytes", "w4a8_linear",
            "w4a8_linear_describe", "w4a8_linear_swiglu", "w4a8_linear_swiglu_workspace_bytes",
            "w4a8_linear_swiglu_describe", "w4a8_rmsnorm_quantize_act", "w4a8_stream_attention",
-           "w4a8_stream_attention_workspace_bytes", "w4a8_flow_schedule", "w4a8_flow_step")
+           "w4a8_stream_attention_workspace_bytes", "w4a8_flow_schedule", "w4a8_flow_step",
+           "w4a8_linear_noalloc")
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 _OUT_DTYPE = {OUT_BF16: torch.bfloat16, OUT_F32: torch.float32, OUT_I32_ACC: torch.int32}
 
@@ -74,6 +76,8 @@ def lib() -> ctypes.CDLL:
         L.w4a8_linear_workspace_bytes.restype = SZ
         L.w4a8_linear.argtypes = [P, I, P, I64, I64, P, P, I, I64, P, I, P, SZ, P]
         L.w4a8_linear.restype = I
+        L.w4a8_linear_noalloc.argtypes = [P, I, P, I64, I64, P, P, I, I64, P, I, P]
+        L.w4a8_linear_noalloc.restype = I
         L.w4a8_linear_describe.argtypes = [I64, I64, I64, I, I, I]
         L.w4a8_linear_describe.restype = ctypes.c_char_p
         L.w4a8_linear_swiglu_workspace_bytes.argtypes = [I64, I64, I64, I, I]
@@ -303,6 +307,33 @@ def w4a8_linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor |
     """
     return _linear_call("w4a8_linear", x, w_packed, w_scale, N, N, x_scale, scale_mode, out_kind, out,
                         workspace, stream)
+
+
+def w4a8_linear_noalloc(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor | None, N: int, *,
+                        x_scale: torch.Tensor | None = None, scale_mode: int = SCALE_CHANNEL_F32,
+                        out_kind: int = OUT_BF16, out: torch.Tensor, stream=None) -> torch.Tensor:
+    """w4a8_linear without a workspace, into a caller-given `out`: the call's
+    scratch memory is the library's own per-GPU array (at most
+    NOALLOC_SCRATCH_BYTES of workspace), so nothing is allocated.  Calls that
+    may overlap on one GPU must not be issued."""
+    M, K = x.shape
+    if x.dtype == torch.bfloat16:
+        in_kind, xs_ptr = IN_BF16, None
+    elif x.dtype == torch.int8:
+        if x_scale is None:
+            raise ValueError("int8 input needs x_scale")
+        in_kind, xs_ptr = IN_I8, _dev(x_scale, "x_scale", torch.float32)
+    else:
+        raise TypeError("x must be bf16 or int8")
+    if tuple(out.shape) != (M, N):
+        raise ValueError(f"out must be [{M}][{N}]")
+    ws_ptr = None if w_scale is None else _dev(
+        w_scale, "w_scale", torch.float32 if scale_mode == SCALE_CHANNEL_F32 else torch.float16)
+    rc = lib().w4a8_linear_noalloc(_dev(x, "x", x.dtype), in_kind, xs_ptr, M, K,
+                                   _dev(w_packed, "w_packed", torch.uint8), ws_ptr, scale_mode, N,
+                                   _dev(out, "out", _OUT_DTYPE[out_kind]), out_kind, _stream(stream))
+    _check(rc, "w4a8_linear_noalloc")
+    return out
 
 
 def w4a8_linear_swiglu_workspace_bytes(M: int, N: int, K: int, scale_mode: int = SCALE_CHANNEL_F32,

@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libw4a8.so")
 SOURCES = ["quantize.hip", "pack.hip", "gemm_smallm.hip", "gemm_largem.hip", "gemm_largem_group.hip",
-           "attention.hip", "flow.hip", "api.cpp"]
+           "attention.hip", "flow.hip", "noalloc.hip", "api.cpp"]
 # per-source extra flags: the group-scale GEMM instances use VGPR-form MFMAs
 EXTRA_FLAGS = {"gemm_largem_group.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

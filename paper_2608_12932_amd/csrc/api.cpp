@@ -14,6 +14,7 @@ using namespace w4a8;
 namespace {
 
 constexpr int64_t kNMax = int64_t(1) << 24;
+static_assert(W4A8_NOALLOC_SCRATCH_BYTES == kNoAllocScratchBytes, "header and library agree on the scratch size");
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -78,10 +79,13 @@ bool gated_shape(int64_t N) { return N % 32 == 0; }
 
 // Both linear entry points after their own checks: the rest of the
 // validation, the plan, and the launches.
+// noalloc: the workspace is this device's library-owned scratch array
+// (workspace and workspace_bytes are ignored); its split-K counters are
+// cleared by a kernel before use.
 w4a8_status run_linear(const void* x, int in_kind, const float* x_scale, int64_t M, int64_t K,
                        const uint8_t* w_packed, const void* w_scale, int scale_mode, int64_t N, void* y,
                        int out_kind, void* workspace, size_t workspace_bytes, hipStream_t stream,
-                       bool swiglu) {
+                       bool swiglu, bool noalloc = false) {
   if (M < 0 || M > W4A8_M_MAX || !valid_nk(N, K)) return W4A8_EINVAL;
   if (!valid_modes(scale_mode, in_kind)) return W4A8_EINVAL;
   if (out_kind != W4A8_OUT_BF16 && out_kind != W4A8_OUT_F32 && out_kind != W4A8_OUT_I32_ACC)
@@ -103,8 +107,19 @@ w4a8_status run_linear(const void* x, int in_kind, const float* x_scale, int64_t
   const bool bf16_in = in_kind == W4A8_IN_BF16;
   const Plan p = make_plan(M, N, K, group, bf16_in, swiglu);
   if (!p.counters_fit || !p.grid_fits) return W4A8_EUNSUPPORTED;
-  if (workspace_bytes < p.total) return W4A8_EINVAL;
-  if (p.total && (!workspace || !aligned(workspace, 256))) return W4A8_EINVAL;
+  if (noalloc) {
+    if (p.total > kNoAllocScratchBytes) return W4A8_EUNSUPPORTED;
+    workspace = nullptr;
+    if (p.total) {
+      if (noalloc_scratch(&workspace) != hipSuccess) return W4A8_EHIP;
+      if (p.small_m && p.sm.S > 1 &&
+          launch_clear_words(static_cast<unsigned*>(workspace), p.sm.groups, stream) != hipSuccess)
+        return W4A8_EHIP;
+    }
+  } else {
+    if (workspace_bytes < p.total) return W4A8_EINVAL;
+    if (p.total && (!workspace || !aligned(workspace, 256))) return W4A8_EINVAL;
+  }
 
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   const void* xin = x;
@@ -327,6 +342,13 @@ w4a8_status w4a8_linear(const void* x, int in_kind, const float* x_scale, int64_
                         hipStream_t stream) {
   return run_linear(x, in_kind, x_scale, M, K, w_packed, w_scale, scale_mode, N, y, out_kind, workspace,
                     workspace_bytes, stream, false);
+}
+
+w4a8_status w4a8_linear_noalloc(const void* x, int in_kind, const float* x_scale, int64_t M, int64_t K,
+                                const uint8_t* w_packed, const void* w_scale, int scale_mode, int64_t N,
+                                void* y, int out_kind, hipStream_t stream) {
+  return run_linear(x, in_kind, x_scale, M, K, w_packed, w_scale, scale_mode, N, y, out_kind, nullptr, 0,
+                    stream, false, true);
 }
 
 size_t w4a8_linear_swiglu_workspace_bytes(int64_t M, int64_t N, int64_t K, int scale_mode, int in_kind) {

@@ -123,6 +123,15 @@ size_t stream_attention_workspace(int H, int Nq, int Nk);
 hipError_t launch_flow_step(float* x, const uint16_t* v, uint16_t* cache, int B, int n, float dt, int repeat,
                             double* stats, hipStream_t stream);
 
+// ---- library-owned scratch of w4a8_linear_noalloc (noalloc.hip)
+// Size of the per-device scratch array; the caller-workspace layout of
+// w4a8_linear (counter region first) is laid over it.
+constexpr size_t kNoAllocScratchBytes = size_t(32) << 20;
+// Device address of this device's scratch array (looked up once per device).
+hipError_t noalloc_scratch(void** ptr);
+// Zero words [0, n) of p with a kernel on `stream`.
+hipError_t launch_clear_words(unsigned* p, int n, hipStream_t stream);
+
 const char* smallm_kernel_name(const SmallMPlan& p);
 const char* largem_kernel_name(const LargeMPlan& p);
 

@@ -239,3 +239,16 @@ def test_largest_shapes_plan_a_grid_that_fits_one_launch(scale_mode):
     assert int(m.group(1)) * int(m.group(2)) < 2 ** 31
     assert w.w4a8_linear_workspace_bytes(M, N, K, scale_mode) >= M * K
 
+
+def test_noalloc_rejects_problems_past_its_scratch_before_any_launch():
+    # bf16 input at M = 4096, K = 65536 needs 256 MiB of codes, more than the
+    # 32 MiB scratch: rejected on the host (the dummy pointers are never used)
+    L = w.lib()
+    p = ctypes.c_void_p(0x10000)
+    M, K, N = 4096, 65536, 16
+    assert w.w4a8_linear_workspace_bytes(M, N, K) > w.NOALLOC_SCRATCH_BYTES
+    rc = L.w4a8_linear_noalloc(p, w.IN_BF16, None, M, K, p, p, w.SCALE_CHANNEL_F32, N, p, w.OUT_BF16, None)
+    assert rc == w.W4A8_EUNSUPPORTED
+    # argument errors come first, as for w4a8_linear; M == 0 is a no-op
+    assert L.w4a8_linear_noalloc(p, w.IN_BF16, None, 16, 100, p, p, 0, N, p, 0, None) == w.W4A8_EINVAL
+    assert L.w4a8_linear_noalloc(p, w.IN_BF16, None, 0, K, p, p, 0, N, p, 0, None) == w.W4A8_OK

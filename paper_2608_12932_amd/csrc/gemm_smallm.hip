@@ -47,6 +47,7 @@ constexpr int kOperandVgprsFused = 112;  // the fused path also holds the x chun
 constexpr int kLdsHeader = 256;   // per-row absmax / s / inv / mode
 constexpr int kMaxTilesPerWave = 12;
 constexpr int kMaxFusedTiles = 2;  // fused quantize pays off up to this many tiles
+constexpr int kFusedMinKB = 256;   // ... and from this many 128-k blocks (K >= 32768) on
 
 // How the activations reach the MFMA A operand.
 enum QMode {
@@ -606,13 +607,16 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in, bool swigl
   int mp = 1;
   while (mp < M) mp *= 2;
   p.tpr = kThreads / (mp < 16 ? mp : 16);
-  // Fused quantize only for narrow column groups over a long K: with NT >= 3
-  // the waves' deeper weight prologue stalls them at issue while the
-  // quantize work is still ahead, and with K < 8192 the activation read
-  // every workgroup makes before its weight stream costs more than the
-  // separate quantize launch (measured on the layer shapes, M = 1..16).
+  // Fused quantize only for narrow column groups over a very long K.  Every
+  // workgroup reads the whole token rows before its weight stream starts,
+  // and that read alone takes ~3.5 us (a timeline of the down projection,
+  // K = 12288, M = 1: rows in at 3.6 us, weights issued from 4.3 us); a
+  // separate quantize launch costs ~3 us, the launch floor being ~2.4 us.
+  // Measured down projection, us per call: M = 1: fused 10.4, separate
+  // 9.5; M = 4: 10.4 against 9.7.  With NT >= 3 the deeper weight prologue
+  // also stalls the waves at issue while the quantize work is still ahead.
   p.qmode = kQNone;
-  if (bf16_in && p.MT == 1 && p.NT <= kMaxFusedTiles && KB >= 64 && (K / 8) % p.tpr == 0 &&
+  if (bf16_in && p.MT == 1 && p.NT <= kMaxFusedTiles && KB >= kFusedMinKB && (K / 8) % p.tpr == 0 &&
       (K / 8) / p.tpr <= kXCache && (size_t)M * (kbs * 128 + 16) <= 96 * 1024)
     p.qmode = kQLds;
   p.fused = p.qmode != kQNone;

@@ -54,9 +54,12 @@ def test_workspace_bytes_plans():
     # gate+up verify: codes from the quantize kernel live in the workspace
     assert w.w4a8_linear_workspace_bytes(16, 24576, 4096) >= 16 * 4096 + 16 * 4
     assert w.w4a8_linear_workspace_bytes(16, 24576, 4096, in_kind=w.IN_I8) == 0
-    # down verify at M=1: quantize fused into the GEMM, no split -> none
-    assert w.w4a8_linear_workspace_bytes(1, 4096, 12288) == 0
-    assert "fused-quant" in w.w4a8_linear_describe(1, 4096, 12288)
+    # down verify at M=1: a quantize launch first, its codes in the workspace
+    assert w.w4a8_linear_workspace_bytes(1, 4096, 12288) >= 64 * 1024 + 12288 + 4
+    assert "quantize_rows + " in w.w4a8_linear_describe(1, 4096, 12288)
+    # very long K over one or two column tiles: quantize fused, no workspace
+    assert w.w4a8_linear_workspace_bytes(1, 32, 32768) == 0
+    assert "fused-quant" in w.w4a8_linear_describe(1, 32, 32768)
     # large M with bf16 input: codes + scales in the workspace
     ws = w.w4a8_linear_workspace_bytes(1024, 6144, 4096)
     assert ws >= 1024 * 4096 + 1024 * 4
@@ -81,17 +84,18 @@ def test_split_and_fusion_choices():
     # K is split across workgroups only where one workgroup's weight stream
     # would be long (one or two column tiles over K = 65536), never at the
     # decoder-layer shapes; the quantize is fused only for narrow column
-    # groups over a long K.
+    # groups over a very long K (never at the layer shapes).
     for K, N in ((4096, 6144), (4096, 4096), (4096, 24576), (12288, 4096)):
         for M in (1, 4, 16, 64):
             for mode in (0, 1):
                 assert "S=1 " in w.w4a8_linear_describe(M, N, K, mode), (M, N, K, mode)
     for M in (1, 16):
         assert "S=8 " in w.w4a8_linear_describe(M, 16, 65536)
-    assert "fused-quant" in w.w4a8_linear_describe(1, 4096, 12288)
-    assert "fused-quant" in w.w4a8_linear_describe(4, 4096, 12288, 1)
-    assert "fused-quant" not in w.w4a8_linear_describe(1, 4096, 4096)
-    assert "fused-quant" not in w.w4a8_linear_describe(16, 6144, 4096)
+    for K, N in ((4096, 6144), (4096, 4096), (4096, 24576), (12288, 4096)):
+        for M in (1, 4, 16):
+            assert "fused-quant" not in w.w4a8_linear_describe(M, N, K), (M, N, K)
+    assert "fused-quant" in w.w4a8_linear_describe(1, 16, 65536)
+    assert "fused-quant" in w.w4a8_linear_describe(2, 32, 32768, 1)
     # group scales use the same column groups as per-channel scales
     assert "NT=6" in w.w4a8_linear_describe(16, 24576, 4096, 1)
 

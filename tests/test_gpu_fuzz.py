@@ -16,8 +16,8 @@ MAX_MACS = 2e9  # about 0.1 s of the oracle on 16 threads
 
 
 def cases(seed=20260812):
-    """Strata: small M with any N, K; the fused quantize (M = 1, 2, 4 with
-    bf16 input over K = 8192..16384 and few columns); K splits (one to four
+    """Strata: small M with any N, K; the fused quantize (M = 1, 2 with
+    bf16 input over K = 32768..65536 and few columns); K splits (one to four
     column tiles over a very long K); large M over few or many columns, so
     that every tile of the menu is drawn."""
     rng = np.random.Generator(np.random.PCG64(seed))
@@ -25,7 +25,7 @@ def cases(seed=20260812):
     strata = [
         (12, lambda: (int(rng.integers(1, 65)), 128 * int(rng.integers(1, 97)), 16 * int(rng.integers(1, 1537))),
          any_codes),
-        (4, lambda: (int(rng.choice([1, 2, 4])), 4096 * int(rng.integers(2, 5)), 16 * int(rng.integers(1, 257))),
+        (4, lambda: (int(rng.choice([1, 2])), 8192 * int(rng.integers(4, 9)), 16 * int(rng.integers(1, 129))),
          lambda: False),
         (4, lambda: (int(rng.integers(1, 17)), 128 * int(rng.integers(256, 513)), 16 * int(rng.integers(1, 5))),
          any_codes),

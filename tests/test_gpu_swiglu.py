@@ -139,8 +139,9 @@ def test_large_m_shapes(M, F, K, codes, seed, group):
     (33, 64, 384, True, 312),      # four 16-row tiles, int8 codes in
     (64, 48, 1024, False, 313),    # the largest M
     (2, 6144, 4096, True, 314),    # NT=4
-    (1, 2048, 12288, False, 315),  # quantize fused into the GEMM
+    (1, 2048, 12288, False, 315),  # the down projection's K, quantize launch first
     (4, 2048, 12288, False, 316),
+    (1, 16, 32768, False, 320),    # quantize fused into the GEMM (very long K)
     (16, 16, 65536, False, 317),   # split K (S=8), separate quantize
     (1, 16, 65536, False, 318),    # split K with the fused quantize
     (16, 16, 65536, True, 319),

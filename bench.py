@@ -62,10 +62,11 @@ def file_hash(name: str) -> str:
         return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
-def counter_traffic(name: str):
-    """HBM bytes per dispatch from a committed rocprofv3 counter summary, or
-    None if there is none or the kernels changed since it was taken."""
-    path = os.path.join(PROFILES, f"{name}_counters.txt")
+def profile_summary(name: str):
+    """The key: value lines of a committed rocprofv3 summary
+    (profiles/<name>.txt), or None if there is none or the kernel sources
+    changed since it was taken."""
+    path = os.path.join(PROFILES, f"{name}.txt")
     if not os.path.exists(path):
         return None
     vals = {}
@@ -76,10 +77,31 @@ def counter_traffic(name: str):
                 vals[k.strip()] = v.strip()
     if vals.get("source_hash") != kernel_source_hash():
         return None
+    return vals
+
+
+def counter_traffic(name: str):
+    """HBM bytes per dispatch of the profiled kernel (FETCH_SIZE + WRITE_SIZE,
+    calibrated), or None."""
+    vals = profile_summary(name)
     try:
-        return float(vals["hbm_bytes_per_dispatch"])
+        return float(vals["hbm_bytes_per_dispatch"]) if vals else None
     except (KeyError, ValueError):
         return None
+
+
+def trace_roofline(name: str, work: float, peak: float, unit_scale: float):
+    """The dominant kernel's roofline from the committed kernel trace: its
+    average duration over the profiled run and the fraction of `peak` that
+    `work` (bytes or ops per launch) in that time gives.  unit_scale turns
+    work per second into the peak's unit."""
+    vals = profile_summary(name)
+    if not vals or "avg_us" not in vals:
+        return None
+    us = float(vals["avg_us"])
+    achieved = work / (us * 1e-6) / unit_scale
+    return {"file": f"profiles/{name}.txt", "kernel": vals.get("kernel"), "avg_us": us,
+            "achieved": round(achieved, 2), "frac": round(achieved / peak, 4)}
 
 
 class DirectCall:
@@ -602,7 +624,8 @@ def bench_stack(steps, layers=36):
         torch.cuda.current_stream().wait_stream(cap)
         ms_graph = time_steps(lambda i: g.replay(), steps, 3)
         rows.append({"M": M, "linears": len(calls), "us_eager": round(ms_eager * 1e3, 1),
-                     "us_graph": round(ms_graph * 1e3, 1), "GB/s_graph": round(nbytes / (ms_graph * 1e-3) / 1e9, 1),
+                     "us_graph": round(ms_graph * 1e3, 1), "us_per_token_graph": round(ms_graph * 1e3 / M, 2),
+                     "GB/s_graph": round(nbytes / (ms_graph * 1e-3) / 1e9, 1),
                      "frac_hbm_graph": round(nbytes / (ms_graph * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "algorithmic_bytes": nbytes})
         del calls, g
@@ -822,7 +845,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(gemm_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gemm_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": w.w4a8_linear_describe(M, N, K, 0, 1), "kernel_ms": round(ms_gemm, 6),
-                     "algorithmic_bytes": gemm_bytes},
+                     "algorithmic_bytes": gemm_bytes,
+                     "timing": "HIP events on the launch stream over back-to-back launches (launch to launch)",
+                     "from_trace": trace_roofline("smallm_gate_up_verify", gemm_bytes, HBM_PEAK_GBS, 1e9)},
     }
     if not args.no_secondary:
         r = bench_qkv(max(50, args.steps // 4), max(10, args.warmup // 4))
@@ -841,7 +866,8 @@ def main():
             "roofline": {"bound": "mfma", "achieved": round(tops_gemm, 2), "peak": INT8_PEAK_TOPS, "unit": "TOPS",
                          "frac": round(tops_gemm / INT8_PEAK_TOPS, 4), "kernel_ms": round(r["ms_gemm"], 6),
                          "kernel": w.w4a8_linear_describe(r["M"], r["N"], r["K"], 0, 1),
-                         "traffic": counter_traffic("largem_qkv_prefill")},
+                         "traffic": counter_traffic("largem_qkv_prefill"),
+                         "from_trace": trace_roofline("largem_qkv_prefill", r["ops"], INT8_PEAK_TOPS, 1e12)},
         }
     out["ceilings"] = measure_ceilings()
     if not args.no_sweep:

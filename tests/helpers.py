@@ -73,10 +73,11 @@ def run_linear(x_bits, wp, s, N, *, group, out_kind, codes=None, workspace=None)
     return y.cpu().numpy()
 
 
-def check_all_outputs(x_bits, W, s, *, group, codes=False, ref=None, rows=None, label=""):
+def check_all_outputs(x_bits, W, s, *, group, codes=False, ref=None, rows=None, label="", wp=None):
     """Run I32 / F32 / BF16 outputs and compare with the oracle.
     rows: optional index array; only those token rows are compared (the
-    oracle computes just them, rows being independent)."""
+    oracle computes just them, rows being independent).  wp: W already
+    packed on the device (packed here otherwise)."""
     M, K = x_bits.shape
     N = W.shape[0]
     print(f"[case] {label} M={M} K={K} N={N} group={group} codes={codes} "
@@ -84,7 +85,8 @@ def check_all_outputs(x_bits, W, s, *, group, codes=False, ref=None, rows=None, 
     if ref is None:
         xs = x_bits if rows is None else x_bits[rows]
         ref = oracle.linear(xs, W, s_w=None if group else s, s_g=s if group else None, nthreads=NTHREADS)
-    wp = pack(W)
+    if wp is None:
+        wp = pack(W)
     cq = None
     if codes:
         qq, ss = oracle.quantize_act(x_bits)

@@ -100,3 +100,56 @@ def test_gated_graph_replays_match_eager(M, F, K, group):
         call()
         torch.cuda.synchronize()
         assert torch.equal(y.view(torch.int16), ref.view(torch.int16)), ("eager", rep)
+
+
+@pytest.mark.parametrize("M,group", [(1, False), (16, False), (1, True), (16, True)])
+def test_replayed_decoder_stack_matches_oracle(M, group):
+    """The backbone's linears of a decode / verify step as one captured HIP
+    graph (the per-stage graph capture of FlashDrive Sec. 3.5): four decoder
+    layers x (QKV, O, gate+up, down) with distinct seeded weights, each call
+    on its own bf16 input.  Every replay, with eager calls between replays,
+    is compared with the oracle linear by linear: per-channel outputs bit for
+    bit, group-scale outputs within the derived tolerance."""
+    import oracle
+    from helpers import GROUP_FLOOR, NTHREADS, REL, to_np_bits
+
+    layers = 4
+    calls = build_calls(M, group, layers=layers)
+    print(f"[case] replayed stack M={M} group={group} linears={len(calls)}", flush=True)
+    refs = []
+    for l in range(layers):
+        for mi, (name, K, N) in enumerate(I.LAYER_MATS):
+            W, s = I.weights(N, K, 1000 + 10 * l + mi, group=group)
+            x = I.activations(M, K, 2000 + 10 * l + mi)
+            refs.append(oracle.linear(x, W, s_w=None if group else s, s_g=s if group else None, nthreads=NTHREADS))
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    run(calls)  # warm the binding's lazy state before capture
+    torch.cuda.synchronize()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            run(calls, stream=cap)
+    torch.cuda.current_stream().wait_stream(cap)
+    torch.cuda.synchronize()
+
+    def check(tag):
+        for i, c in enumerate(calls):
+            got = to_np_bits(c[4])
+            ref = refs[i]
+            if not group:
+                np.testing.assert_array_equal(got, ref["y"], err_msg=f"{tag} linear {i}")
+            else:
+                yf = (got.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+                bound = REL * np.abs(ref["y64"]) + GROUP_FLOOR * ref["bound"]
+                assert np.all(np.abs(yf - ref["y64"]) <= bound), f"{tag} linear {i}"
+
+    for rep in range(3):
+        for c in calls:
+            c[4].fill_(1.0)
+        g.replay()
+        torch.cuda.synchronize()
+        check(f"replay {rep}")
+        run(calls)
+        torch.cuda.synchronize()
+        check(f"eager {rep}")

@@ -724,6 +724,25 @@ def measure_ceilings():
                           "what": "4 independent v_mfma_i32_32x32x32_i8 chains per wave, 4096 waves"}}
 
 
+def library_int8_gemm(M=1024, N=6144, K=4096, steps=50, warmup=10):
+    """The vendor library's plain int8 GEMM at the qkv prefill shape, for
+    context: torch._int_mm (hipBLASLt) on int8 activations [M][K] and 8-bit
+    weights stored [N][K] (passed as the transposed view), int32 out.  It
+    reads twice the weight bytes of the 4-bit path and applies no scales."""
+    import torch
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2608)
+    a = torch.randint(-127, 128, (M, K), dtype=torch.int8, device="cuda", generator=g)
+    b = torch.randint(-8, 8, (N, K), dtype=torch.int8, device="cuda", generator=g)
+    bt = b.t()
+    ms = time_steps(lambda i: torch._int_mm(a, bt), steps, warmup)
+    tops = 2.0 * M * N * K / (ms * 1e-3) / 1e12
+    return {"value": round(tops, 1), "unit": "TOPS", "us": round(ms * 1e3, 3),
+            "frac_of_peak": round(tops / INT8_PEAK_TOPS, 4),
+            "what": f"torch._int_mm (hipBLASLt) int8 x int8 -> int32, M={M} N={N} K={K}, 8-bit weights, no scales"}
+
+
 def host_cpu():
     """The host's logical CPU count, the CPUs this process may run on, and
     the CPU model name (from /proc/cpuinfo, as lscpu reports it)."""
@@ -870,6 +889,13 @@ def main():
                          "from_trace": trace_roofline("largem_qkv_prefill", r["ops"], INT8_PEAK_TOPS, 1e12)},
         }
     out["ceilings"] = measure_ceilings()
+    try:
+        out["ceilings"]["library_int8_gemm"] = library_int8_gemm()
+        if "secondary" in out:
+            out["secondary"]["roofline"]["speedup_vs_library_int8_gemm"] = round(
+                out["ceilings"]["library_int8_gemm"]["us"] / (out["secondary"]["roofline"]["kernel_ms"] * 1e3), 3)
+    except RuntimeError as e:  # torch built without the int8 GEMM
+        out["ceilings"]["library_int8_gemm"] = {"error": str(e)[:200]}
     if not args.no_sweep:
         ss, sw = max(50, args.steps // 4), max(10, args.warmup // 4)
         out["sweep"] = {"down_verify": bench_down_verify(ss, sw), "gate_up_swiglu": bench_gate_up_swiglu(ss, sw),

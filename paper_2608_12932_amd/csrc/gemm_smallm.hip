@@ -222,10 +222,25 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   // with a short split, D can exceed the blocks a wave owns.  Group mode
   // issues them (they read zeros): guarding its loads made the compiler
   // spill the stage registers.
+  // Issue order across the waves: the CU serves vector-memory requests
+  // roughly in issue order, so a wave that issues its whole prologue at
+  // once gets all of its blocks before the next wave gets any, and the last
+  // waves then compute after the stream has ended.  A workgroup barrier
+  // after stage s sends every wave's copy of stages 0 .. s ahead of the
+  // rest.  Measured, us per call on int8 codes (none / after every stage /
+  // after stage 0): down M = 1 6.35 / 6.30 / 6.46; O group M = 1
+  // 5.28 / 4.84 / 5.24; qkv group M = 16 6.58 / 6.55 / 6.40; gate+up group
+  // M = 1 10.9 / 10.9 / 10.16, M = 16 11.6 / 11.46 / 11.04; gate+up
+  // channel M = 16 10.87 / 11.27 / 11.03.  So one column tile per wave takes
+  // a barrier after every stage, the other group instances one after stage
+  // 0, and the other per-channel instances none.
+  constexpr int kIssueBarriers = NT == 1 ? D - 1 : (GROUP ? 1 : 0);
   if constexpr (QM != kQLds) {
 #pragma unroll
-    for (int s = 0; s < D; ++s)
+    for (int s = 0; s < D; ++s) {
       if (EXACT || GROUP || s < iters) load_stage(s, s);
+      if (s < kIssueBarriers) __builtin_amdgcn_s_barrier();
+    }
   }
 
   // ---- epilogue scales, fetched now so their latency hides under the
@@ -555,21 +570,36 @@ SmallMKernel pick(const SmallMPlan& p) {
 
 }  // namespace
 
-// Plan cost model, fitted to measurements of the layer shapes at M = 1..16:
-// a call takes about
-//   (rounds - 1) * kRoundUs + max(all bytes / kHbmGBs, rounds * bytes per workgroup / kCuGBs)
+// Plan cost model.  Candidates (column tiles per workgroup NT, K splits S)
+// are compared on
+//   (rounds - 1) * kRoundUs
+//   + max(all bytes / kHbmGBs, rounds * bytes per workgroup / kCuGBs)
 //   + kSplitUs if K is split,
-// where rounds = workgroup rounds over the 256 CUs.  One workgroup streams
-// at most ~60 GB/s, the whole chip ~6.5 TB/s; a second round of workgroups
-// costs its own ramp-up and drain; a K split adds a serial chain (partial
-// stores, the arrival counter, the finishing workgroup's reads).  With the
-// layer shapes this keeps S = 1 (the partial-sum handoff never pays off
-// below ~400 KB of weights per workgroup) and picks the narrowest column
-// group that still fits one round.
+// where rounds = workgroup rounds over the 256 CUs and a workgroup's bytes
+// are its packed weights plus half of the activation codes it reads.  The
+// whole chip streams ~6.5 TB/s, one workgroup at most ~60 GB/s; a second
+// round of workgroups costs its own ramp-up and drain; a K split adds a
+// serial chain (partial stores, the arrival counter, the finishing
+// workgroup's reads).  With the layer shapes this keeps S = 1 (the
+// partial-sum handoff never pays off below ~400 KB of weights per
+// workgroup) and picks the narrowest column group that still fits one
+// round; the split choices were checked on the GPU at K = 65536.
+// The launch's estimated time (SmallMPlan::model_us, shown by the plan
+// description) adds what every candidate pays alike, or what was measured
+// only without a split:
+//   kFixedUs (dispatch, the first bytes' latency, the wave reduction and
+//   epilogue, the drain) + the workgroup's codes / kActGBs (read from L2
+//   beyond the weight stream) + kGroupUs with group scales (their
+//   scattered loads and the rescale).
+// Against the kernel-trace averages of the layer shapes (gate+up, qkv, O,
+// down at M = 1, 4, 16, both scale modes) the estimate is within ~13 %.
 constexpr double kRoundUs = 1.5;
 constexpr double kHbmGBs = 6500.0;
 constexpr double kCuGBs = 60.0;
 constexpr double kSplitUs = 5.0;
+constexpr double kFixedUs = 3.2;
+constexpr double kActGBs = 70.0;
+constexpr double kGroupUs = 1.0;
 
 SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in, bool swiglu) {
   SmallMPlan p{};
@@ -591,7 +621,8 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in, bool swigl
       const long rounds = (wgs + 255) / 256;
       // weights, plus the activation codes every workgroup reads (from L2,
       // counted at half weight)
-      const double wg_bytes = (double)nt * kbs * kBlockBytes + 0.5 * (double)M * kbs * 128;
+      const double codes = (double)M * kbs * 128;
+      const double wg_bytes = (double)nt * kbs * kBlockBytes + 0.5 * codes;
       double us = (double)(rounds - 1) * kRoundUs +
                   fmax(all_bytes / (kHbmGBs * 1e3), (double)rounds * wg_bytes / (kCuGBs * 1e3));
       if (s > 1) us += kSplitUs;
@@ -600,6 +631,7 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in, bool swigl
         p.NT = nt;
         p.S = s;
         p.groups = ntiles / nt;
+        p.model_us = us + kFixedUs + codes / (kActGBs * 1e3) + (group ? kGroupUs : 0.0);
       }
     }
   }
@@ -645,10 +677,10 @@ hipError_t launch_smallm(const SmallMPlan& p, const SmallMArgs& a, hipStream_t s
 }
 
 const char* smallm_kernel_name(const SmallMPlan& p) {
-  static thread_local char buf[96];
+  static thread_local char buf[128];
   static const char* modes[] = {"int8-in", "fused-quant"};
-  snprintf(buf, sizeof buf, "smallm<MT=%d,NT=%d,%s,%s%s> S=%d groups=%d", p.MT, p.NT,
-           p.group ? "group" : "channel", modes[p.qmode], p.swiglu ? ",swiglu" : "", p.S, p.groups);
+  snprintf(buf, sizeof buf, "smallm<MT=%d,NT=%d,%s,%s%s> S=%d groups=%d model=%.1fus", p.MT, p.NT,
+           p.group ? "group" : "channel", modes[p.qmode], p.swiglu ? ",swiglu" : "", p.S, p.groups, p.model_us);
   return buf;
 }
 

@@ -54,6 +54,7 @@ struct SmallMPlan {
   bool exact;            // every wave's block count is a multiple of the stage depth
   bool swiglu;           // gated output silu(gate) * up (gate columns [0, N/2), up [N/2, N))
   size_t lds_bytes;
+  double model_us;       // the cost model's time for the GEMM launch (int8 codes in)
 };
 SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in, bool swiglu);
 hipError_t launch_smallm(const SmallMPlan& p, const SmallMArgs& a, hipStream_t stream);

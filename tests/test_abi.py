@@ -256,3 +256,33 @@ def test_noalloc_rejects_problems_past_its_scratch_before_any_launch():
     # argument errors come first, as for w4a8_linear; M == 0 is a no-op
     assert L.w4a8_linear_noalloc(p, w.IN_BF16, None, 16, 100, p, p, 0, N, p, 0, None) == w.W4A8_EINVAL
     assert L.w4a8_linear_noalloc(p, w.IN_BF16, None, 0, K, p, p, 0, N, p, 0, None) == w.W4A8_OK
+
+
+# The small-M plan's time estimate (the "model=" field of the description)
+# against the committed rocprofv3 kernel-trace averages of the layer shapes
+# (int8 codes in).  A summary taken before the kernel sources last changed
+# is skipped.
+SMALLM_PROFILES = [
+    ("smallm_gate_up_verify", "avg_us", (16, 24576, 4096, 0)),
+    ("smallm_down_verify_m1", "avg_us", (1, 4096, 12288, 0)),
+    ("smallm_down_verify_m4", "avg_us", (4, 4096, 12288, 0)),
+    ("smallm_down_verify_m16", "avg_us", (16, 4096, 12288, 0)),
+] + [(f"smallm_group_layer_m{M}", f"{name}.avg_us", (M, N, K, 1))
+     for M in (1, 16)
+     for name, N, K in (("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 24576, 4096), ("down", 4096, 12288))]
+
+
+@pytest.mark.parametrize("profile,key,shape", SMALLM_PROFILES)
+def test_smallm_time_estimate_matches_profile(profile, key, shape):
+    import sys
+    sys.path.insert(0, ROOT)
+    import bench
+
+    vals = bench.profile_summary(profile)
+    if vals is None:
+        pytest.skip(f"profiles/{profile}.txt was taken with other kernel sources")
+    measured = float(vals[key])
+    M, N, K, mode = shape
+    d = w.w4a8_linear_describe(M, N, K, mode, 1)
+    est = float(re.search(r"model=([0-9.]+)us", d).group(1))
+    assert abs(est - measured) <= 0.2 * measured, (d, measured)

@@ -22,6 +22,11 @@
 //     clock then fall on 16 distinct 16-byte bank groups (a swizzle on r & 7
 //     left rows r and r + 8 on the same banks and halved the read rate).
 //     Weight chunks keep the packed order, already conflict free;
+//   - the ring keeps the activation tiles of its 4 stages together, then
+//     their weight tiles, then their scales, and the step loop is unrolled
+//     over the 4 stages: every operand read is one per-lane address plus
+//     the stage's immediate offset, with no address arithmetic in the loop
+//     (3-9 % faster than per-stage blocks with the stage added per read);
 //   - the operands of step kb + 1 are read from LDS into a second register
 //     set between the MFMAs of step kb (v_mfma_i32_32x32x32_i8), and every
 //     other instruction of a step (stage fill, LDS reads, nibble unpack) is
@@ -80,6 +85,12 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   constexpr int kABytes = BM * 128, kBBytes = BN / 16 * kBlockBytes;
   constexpr int kSBytes = GROUP ? kWaves * 256 : 0;  // group scales: 256 B per wave
   constexpr int kStage = kABytes + kBBytes + kSBytes;
+  // LDS: the activation tiles of all ring stages first, then the weight
+  // tiles, then the group scales, so that an operand read is one per-lane
+  // address plus the stage's immediate offset (the activation region of a
+  // 4-deep ring of 128-row tiles is exactly 64 KiB, the immediate's range).
+  constexpr int kAReg = kRing * kABytes, kBReg = kRing * kBBytes;
+  static_assert(kRing == 4, "the step loop is unrolled over the 4 ring stages");
   constexpr int kACh = kABytes / 16 / kThreads, kBCh = kBBytes / 16 / kThreads;  // loads per thread per stage
   static_assert(kACh * kThreads * 16 == kABytes, "A tile must split evenly over the threads");
   static_assert(kBCh * kThreads * 16 == kBBytes, "B tile must split evenly over the threads");
@@ -156,17 +167,17 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   }
   // A step past the end gets the scalar offset kOOB: every lane's offset
   // then lies past the descriptor's range (no vector select needed).
-  auto issue_one = [&](int kb, int d) {
+  auto issue_one = [&](int kb, int stage, int d) {
     const bool ok = kb < KB;
-    const uint32_t st = lds_base + (uint32_t)((kb % kRing) * kStage);
     if (d < kACh) {
-      lds_dma16(ares, st + (d * kWaves + wave) * 1024, a_voff[d], ok ? kb * 128 : kOOB);
+      lds_dma16(ares, lds_base + (uint32_t)(stage * kABytes + (d * kWaves + wave) * 1024), a_voff[d],
+                ok ? kb * 128 : kOOB);
     } else if (d < kACh + kBCh) {
       const int blk = (d - kACh) * kWaves + wave;
-      lds_dma16_nt(b_up[d - kACh] ? bres_u : bres, st + kABytes + blk * 1024, b_voff[d - kACh],
-                   ok ? kb * kBlockBytes : kOOB);
+      lds_dma16_nt(b_up[d - kACh] ? bres_u : bres, lds_base + (uint32_t)(kAReg + stage * kBBytes + blk * 1024),
+                   b_voff[d - kACh], ok ? kb * kBlockBytes : kOOB);
     } else if constexpr (GROUP) {
-      lds_dma4(s_up ? sres_u : sres, st + kABytes + kBBytes + wave * 256, s_voff,
+      lds_dma4(s_up ? sres_u : sres, lds_base + (uint32_t)(kAReg + kBReg + stage * kSBytes + wave * 256), s_voff,
                ok ? (uint32_t)((size_t)kb * N * 2) : kOOB);
     }
   };
@@ -187,7 +198,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
   for (int j = 0; j < WN; ++j) {
     const int col = tile_col(j);
-    b_rd[j] = (uint32_t)(kABytes + (col >> 4) * kBlockBytes + (col & 15) * 16);
+    b_rd[j] = (uint32_t)(kAReg + (col >> 4) * kBlockBytes + (col & 15) * 16);
   }
   // MFMA k half tp covers the 64 k of chunk group g = 2 tp + g2: activation
   // chunks 2 g and 2 g + 1, weight chunk g (low nibbles, then high nibbles).
@@ -198,11 +209,16 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
     a_ch[2 * tp] = (uint32_t)(((2 * g) ^ swz) << 4);
     a_ch[2 * tp + 1] = (uint32_t)(((2 * g + 1) ^ swz) << 4);
   }
+  uint32_t a_addr[WM][4];
+#pragma unroll
+  for (int i = 0; i < WM; ++i)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) a_addr[i][c] = a_rd[i] + a_ch[c];
   uint32_t s_rd[GROUP ? WN : 1];
 #pragma unroll
   for (int j = 0; j < (GROUP ? WN : 1); ++j) {
     const int col = tile_col(j);
-    s_rd[j] = (uint32_t)(kABytes + kBBytes + (col / kSPerWave) * 256 + (col % kSPerWave) * 2);
+    s_rd[j] = (uint32_t)(kAReg + kBReg + (col / kSPerWave) * 256 + (col % kSPerWave) * 2);
   }
 
   // One step's MFMA operands, held in registers so that the LDS reads of
@@ -219,28 +235,30 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   // LDS read r of step kb's operands: per k half the weight chunks first
   // (half 0's are unpacked while the previous step still runs), then the
   // activation chunks; the group scales last.
-  auto read_one = [&](int kb, int r, Ops& o) {
-    const uint8_t* st = lds + (kb % kRing) * kStage;
+  // (stage_c: the ring stage, a compile-time constant, so that its offset
+  // is the instruction's immediate)
+  auto read_one = [&](auto stage_c, int r, Ops& o) {
+    constexpr int S = decltype(stage_c)::value;
     if (r < 2 * kReadsTp) {
       const int tp = r / kReadsTp, u = r % kReadsTp;
       if (u < WN)
-        o.b[u][tp] = *reinterpret_cast<const uint4*>(st + b_rd[u] + (2 * tp + g2) * 256);
+        o.b[u][tp] = *reinterpret_cast<const uint4*>(lds + S * kBBytes + b_rd[u] + (2 * tp + g2) * 256);
       else if constexpr (GROUP) {
         // Group mode reads the activation operands straight into AGPRs
         // (only the MFMA reads them), which leaves the VGPRs to the int32
         // partial sums the rescale reads.  They are used in the next step,
         // whose barrier waits for every outstanding LDS read.
-        const uint32_t addr = (uint32_t)(uintptr_t)(st + a_rd[(u - WN) / 2] + a_ch[2 * tp + ((u - WN) & 1)]);
+        const uint32_t addr = lds_base + a_addr[(u - WN) / 2][2 * tp + ((u - WN) & 1)];
         v4i t;
-        asm volatile("ds_read_b128 %0, %1" : "=a"(t) : "v"(addr) : "memory");
+        asm volatile("ds_read_b128 %0, %1 offset:%2" : "=a"(t) : "v"(addr), "i"(S * kABytes) : "memory");
         o.a[(u - WN) / 2][2 * tp + ((u - WN) & 1)] = t;
       } else {
         o.a[(u - WN) / 2][2 * tp + ((u - WN) & 1)] =
-            *reinterpret_cast<const v4i*>(st + a_rd[(u - WN) / 2] + a_ch[2 * tp + ((u - WN) & 1)]);
+            *reinterpret_cast<const v4i*>(lds + S * kABytes + a_addr[(u - WN) / 2][2 * tp + ((u - WN) & 1)]);
       }
     } else if constexpr (GROUP) {
       const int j = r - 2 * kReadsTp;
-      o.sg[j] = f16_to_f32(*reinterpret_cast<const uint16_t*>(st + s_rd[j])) * 0.0625f;
+      o.sg[j] = f16_to_f32(*reinterpret_cast<const uint16_t*>(lds + S * kSBytes + s_rd[j])) * 0.0625f;
     }
   };
 
@@ -334,7 +352,8 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   float sg_prev[GROUP ? WN : 1];
 #pragma unroll
   for (int j = 0; j < (GROUP ? WN : 1); ++j) sg_prev[j] = 0.0f;
-  auto step = [&](int kb, const Ops& cur, Ops& nxt, v16i (&c)[WM][WN], v16i (&prev)[WM][WN]) {
+  auto step = [&](auto stage_c, int kb, const Ops& cur, Ops& nxt, v16i (&c)[WM][WN], v16i (&prev)[WM][WN]) {
+    constexpr int S = decltype(stage_c)::value;
     wait_vmcnt<(kRing - 2) * kPerStage>();
     lds_barrier();
     v4i lo1[WN], hi1[WN];
@@ -351,10 +370,10 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
         c[i][j] = mfma32(cur.a[i][2 * tp + h], bop, c[i][j]);
 #pragma unroll
       for (int d = 0; d < kPerStage; ++d)
-        if (d * kMfma / kPerStage == q) issue_one(kb + kRing, d);
+        if (d * kMfma / kPerStage == q) issue_one(kb + kRing, S, d);
 #pragma unroll
       for (int r = 0; r < kReads; ++r)
-        if (r * kMfma / kReads == q) read_one(kb + 1, r, nxt);
+        if (r * kMfma / kReads == q) read_one(std::integral_constant<int, (S + 1) % kRing>{}, r, nxt);
 #pragma unroll
       for (int u = 0; u < kUnits; ++u) {
         if (q < kHalf && u * kHalf / kUnits == q) unpack_word(cur.b[u / 4][1], u % 4, lo1[u / 4], hi1[u / 4]);
@@ -399,7 +418,8 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   float sg_last[GROUP ? WN : 1];
 #pragma unroll
   for (int j = 0; j < (GROUP ? WN : 1); ++j) sg_last[j] = 0.0f;
-  auto step1 = [&](int kb, const Ops& cur, Ops& nxt, v16i (&c)[WM][WN]) {
+  auto step1 = [&](auto stage_c, int kb, const Ops& cur, Ops& nxt, v16i (&c)[WM][WN]) {
+    constexpr int S = decltype(stage_c)::value;
     wait_vmcnt<(kRing - 2) * kPerStage>();
     lds_barrier();
 #pragma unroll
@@ -413,10 +433,10 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
         c[i][j] = mfma32(cur.a[i][2 * tp + h], bop, c[i][j]);
 #pragma unroll
       for (int d = 0; d < kPerStage; ++d)
-        if (d * kMfma / kPerStage == q) issue_one(kb + kRing, d);
+        if (d * kMfma / kPerStage == q) issue_one(kb + kRing, S, d);
 #pragma unroll
       for (int r = 0; r < kReads; ++r)
-        if (r * kMfma / kReads == q) read_one(kb + 1, r, nxt);
+        if (r * kMfma / kReads == q) read_one(std::integral_constant<int, (S + 1) % kRing>{}, r, nxt);
 #pragma unroll
       for (int u = 0; u < kUnits; ++u) {
         if (q == kMfma * 3 / 16 + u * (kMfma * 6 / 16) / kUnits)
@@ -434,28 +454,32 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
   for (int st = 0; st < kRing; ++st)
 #pragma unroll
-    for (int d = 0; d < kPerStage; ++d) issue_one(st, d);
+    for (int d = 0; d < kPerStage; ++d) issue_one(st, st, d);
   Ops o0, o1;
   wait_vmcnt<(kRing - 1) * kPerStage>();  // stage 0 (and the scales, issued before it)
   lds_barrier();
 #pragma unroll
-  for (int r = 0; r < kReads; ++r) read_one(0, r, o0);
+  for (int r = 0; r < kReads; ++r) read_one(std::integral_constant<int, 0>{}, r, o0);
 #pragma unroll
   for (int u = 0; u < kUnits; ++u) unpack0(o0, u);
   if constexpr (GROUP && kMfma >= 12) {
 #pragma unroll
     for (int u = 0; u < kUnits; ++u) unpack_word(o0.b[u / 4][1], u % 4, o0.lo1[u / 4], o0.hi1[u / 4]);
-    for (int kb = 0; kb < KB; kb += 2) {
-      step1(kb, o0, o1, acc[0]);
-      if (kb + 1 < KB) step1(kb + 1, o1, o0, acc[0]);
+    for (int kb = 0; kb < KB; kb += kRing) {
+      step1(std::integral_constant<int, 0>{}, kb, o0, o1, acc[0]);
+      if (kb + 1 < KB) step1(std::integral_constant<int, 1>{}, kb + 1, o1, o0, acc[0]);
+      if (kb + 2 < KB) step1(std::integral_constant<int, 2>{}, kb + 2, o0, o1, acc[0]);
+      if (kb + 3 < KB) step1(std::integral_constant<int, 3>{}, kb + 3, o1, o0, acc[0]);
     }
     // the last step's rescales that fall past its last slot
 #pragma unroll
     for (int q = 0; q < kMfma; ++q) rescale_slot(q, true, acc[0], sg_last);
   } else {
-    for (int kb = 0; kb < KB; kb += 2) {
-      step(kb, o0, o1, acc[0], acc[GROUP ? 1 : 0]);
-      if (kb + 1 < KB) step(kb + 1, o1, o0, acc[GROUP ? 1 : 0], acc[0]);
+    for (int kb = 0; kb < KB; kb += kRing) {
+      step(std::integral_constant<int, 0>{}, kb, o0, o1, acc[0], acc[GROUP ? 1 : 0]);
+      if (kb + 1 < KB) step(std::integral_constant<int, 1>{}, kb + 1, o1, o0, acc[GROUP ? 1 : 0], acc[0]);
+      if (kb + 2 < KB) step(std::integral_constant<int, 2>{}, kb + 2, o0, o1, acc[0], acc[GROUP ? 1 : 0]);
+      if (kb + 3 < KB) step(std::integral_constant<int, 3>{}, kb + 3, o1, o0, acc[GROUP ? 1 : 0], acc[0]);
     }
   }
   if constexpr (GROUP && kMfma < 12) {

@@ -151,6 +151,23 @@ def test_group_scales(M, K, N):
     check_all_outputs(x, W, s, group=True, label="group")
 
 
+# The large-M step loop runs over a 4-stage LDS ring, four steps per
+# iteration: every remainder of the step count (K / 128 mod 4), and counts
+# below and above one iteration, with each tile size the planner picks
+# (64x64 at few tiles, 128x128, 128x192) and ragged row and column tails.
+@pytest.mark.parametrize("M,K,N", [(70, 128, 96), (130, 256, 160), (200, 384, 64), (129, 640, 128),
+                                   (257, 768, 96), (300, 896, 1040), (65, 1280, 48),
+                                   (2048, 128, 4096), (2048, 256, 4096), (2048, 384, 4096), (2048, 640, 4096),
+                                   (2000, 768, 4080), (2048, 896, 4096),
+                                   (1024, 256, 6144), (1024, 384, 6144), (1024, 1152, 6144)])
+@pytest.mark.parametrize("group", [False, True])
+def test_large_m_every_ring_remainder(M, K, N, group):
+    x = I.activations(M, K, 800 + M)
+    W, s = I.weights(N, K, 900 + N, group=group)
+    assert "largem" in w.w4a8_linear_describe(M, N, K, int(group))
+    check_all_outputs(x, W, s, group=group, label="large-M ring remainder")
+
+
 # ------------------------------------------------------------ split-K, determinism, workspace reuse
 
 @pytest.mark.parametrize("M,N", [(16, 32), (1, 16)])

@@ -48,6 +48,9 @@ constexpr int kLdsHeader = 256;   // per-row absmax / s / inv / mode
 constexpr int kMaxTilesPerWave = 12;
 constexpr int kMaxFusedTiles = 2;  // fused quantize pays off up to this many tiles
 constexpr int kFusedMinKB = 256;   // ... and from this many 128-k blocks (K >= 32768) on
+// LDS words per wave tile of partial sums in the reduction: 256 plus a
+// 16-word skew, so that consecutive tiles start 16 banks apart
+constexpr int kRedTile = 272;
 
 // How the activations reach the MFMA A operand.
 enum QMode {
@@ -407,19 +410,25 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   // the middle of the last stages' MFMAs, which cost 0.66 us on gate+up.
   uint32_t* red = reinterpret_cast<uint32_t*>(
       l_body + (QM == kQLds ? ((size_t)M * (a.kbs * 128 + 16) + 15) / 16 * 16 : 0));
+  // Lane l holds rows 4 (l >> 4) + i (i < 4) of column l & 15 of each 16 x
+  // 16 tile; value i goes to word i 64 + l of the wave's tile, so that the
+  // reads below (one row, consecutive columns across the lanes) are
+  // consecutive words, and the skewed tile pitch spreads neighbouring tiles
+  // over the banks.  (Each lane's four values as one 16-byte write left
+  // every column four words apart and every tile on the same banks: 4-way
+  // conflicts on every read of the reduction.)
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      uint4 v;
-      if constexpr (GROUP) {
-        v = make_uint4(__float_as_uint(facc[mt][t][0]), __float_as_uint(facc[mt][t][1]),
-                       __float_as_uint(facc[mt][t][2]), __float_as_uint(facc[mt][t][3]));
-      } else {
-        v = make_uint4((uint32_t)acc[mt][t][0], (uint32_t)acc[mt][t][1], (uint32_t)acc[mt][t][2],
-                       (uint32_t)acc[mt][t][3]);
+      uint32_t* dst = red + ((wave * MT + mt) * NT + t) * kRedTile + lane;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if constexpr (GROUP)
+          dst[i * 64] = __float_as_uint(facc[mt][t][i]);
+        else
+          dst[i * 64] = (uint32_t)acc[mt][t][i];
       }
-      *reinterpret_cast<uint4*>(red + ((wave * MT + mt) * NT + t) * 256 + lane * 4) = v;
     }
   lds_barrier();
 
@@ -427,13 +436,13 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
   auto wave_sum_f = [&](int mt, int t, int src) {
     float v = 0.0f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) v += __uint_as_float(red[((w * MT + mt) * NT + t) * 256 + src]);
+    for (int w = 0; w < kWaves; ++w) v += __uint_as_float(red[((w * MT + mt) * NT + t) * kRedTile + src]);
     return v * 0.0625f;  // every partial and sum above is 16x the true one: exact barring underflow
   };
   auto wave_sum_i = [&](int mt, int t, int src) {
     int v = 0;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) v += (int)red[((w * MT + mt) * NT + t) * 256 + src];
+    for (int w = 0; w < kWaves; ++w) v += (int)red[((w * MT + mt) * NT + t) * kRedTile + src];
     return v;
   };
 #pragma unroll
@@ -443,7 +452,7 @@ __global__ __launch_bounds__(kThreads) void smallm(const SmallMArgs a) {
     const int mt = row >> 4, rr = row & 15, t = col >> 4, cc = col & 15;
     if (o >= kOut || row >= M || t >= tiles_here) continue;
     if constexpr (FUSED) sxp[q] = l_s[row];
-    const int src = ((rr >> 2) * 16 + cc) * 4 + (rr & 3);
+    const int src = (rr & 3) * 64 + (rr >> 2) * 16 + cc;
     const int n = (t0 + t) * 16 + cc;      // (gate) column
     const int nu = (u0 + t) * 16 + cc;     // up column (gated instances)
     if constexpr (GROUP) {
@@ -662,7 +671,7 @@ SmallMPlan plan_smallm(int M, int N, int K, bool group, bool bf16_in, bool swigl
     const int it_full = (kbs + kWaves - 1) / kWaves, it_last = (last + kWaves - 1) / kWaves;
     p.exact = !group && it_full % D == 0 && it_last % D == 0;
   }
-  const size_t red = (size_t)kWaves * p.MT * p.NT * 1024;
+  const size_t red = (size_t)kWaves * p.MT * p.NT * kRedTile * 4;
   const size_t codes = p.qmode == kQLds ? ((size_t)M * (kbs * 128 + 16) + 15) / 16 * 16 : 0;
   p.lds_bytes = kLdsHeader + codes + red;
   return p;

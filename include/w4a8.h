@@ -184,12 +184,13 @@ w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, 
  *   scale        finite (e.g. 1/sqrt(D))
  *   o            device, bf16 [H][Nq][D], 16-byte aligned
  *   workspace    device, >= w4a8_stream_attention_workspace_bytes(H, Nq, Nk)
- *                bytes, 256-byte aligned (may be NULL if that is 0): the
- *                partial results of key-range splits, written before read
- *                (no zero fill needed), past the first 64 KiB, which this
- *                call leaves untouched, so that it may share one buffer
- *                with w4a8_linear's workspace; concurrent calls must not
- *                share it
+ *                bytes, 256-byte aligned: the keys rotated at their
+ *                positions (computed once per call, read by every query
+ *                head of their kv head) and the partial results of
+ *                key-range splits, all written before read (no zero fill
+ *                needed), past the first 64 KiB, which this call leaves
+ *                untouched, so that it may share one buffer with
+ *                w4a8_linear's workspace; concurrent calls must not share it
  * A query that sees no key gets 0.  Does not synchronize; enqueues kernels
  * only.
  */
@@ -198,8 +199,8 @@ w4a8_status w4a8_stream_attention(const uint16_t* q, const uint16_t* k, const ui
                                   int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk, int64_t D, float scale, uint16_t* o,
                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Workspace bytes w4a8_stream_attention needs (0 if none, and 0 for shapes
- * it rejects). */
+/* Workspace bytes w4a8_stream_attention needs (0 for shapes it rejects;
+ * every accepted shape needs some: the rotated keys). */
 size_t w4a8_stream_attention_workspace_bytes(int64_t H, int64_t Nq, int64_t Nk);
 
 /*

@@ -307,7 +307,7 @@ w4a8_status w4a8_stream_attention(const uint16_t* q, const uint16_t* k, const ui
       !aligned(rope_sin, 16))
     return W4A8_EINVAL;
   const size_t need = stream_attention_workspace((int)H, (int)Nq, (int)Nk);
-  if (workspace_bytes < need || (need && (!workspace || !aligned(workspace, 256)))) return W4A8_EINVAL;
+  if (workspace_bytes < need || !workspace || !aligned(workspace, 256)) return W4A8_EINVAL;
   AttnArgs a{};
   a.workspace = workspace;
   a.q = q;

@@ -10,7 +10,9 @@
 // seen by query i exactly when pos_k[j] <= pos_q[i], i.e. causally in the
 // view-major order of the window.
 //
-// One workgroup per (64 queries, head); each of its 4 waves owns 16
+// A first kernel rotates the window's keys once per call, at the
+// positions they occupy now (every query head of a kv head reads them).
+// Then one workgroup per (64 queries, head); each of its 4 waves owns 16
 // queries.  Key tiles that none of its queries can see are skipped.  Per
 // 32-key tile:
 //   - the workgroup stages the rotated keys (bf16, [key][d]) and the values
@@ -71,6 +73,26 @@ __device__ __forceinline__ void rotate_chunks(uint4 a8, uint4 b8, const float* c
   }
   lo = make_uint4(lw[0], lw[1], lw[2], lw[3]);
   hi = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+}
+
+// The keys rotated at their window positions: k_rot[hk][j] from k[hk][j]
+// and pos_k[j], one 16-byte pair of chunks (d = 8 c .., 64 + 8 c ..) per
+// thread, 32 keys of one kv head per workgroup.  Rotating each key once
+// here instead of in every workgroup that stages it (all query blocks of
+// the kv head's query heads) took 21 us off the bench workload's 114 us.
+__global__ __launch_bounds__(256) void rotate_keys(const AttnArgs a) {
+  const int tid = threadIdx.x, hk = blockIdx.y;
+  const int j = blockIdx.x * kKeys + (tid >> 3), c = tid & 7;
+  if (j >= a.Nk) return;
+  const int P = a.n_pos, p = a.pos_k[j];
+  const int pc = p < 0 ? 0 : (p >= P ? P - 1 : p);  // table reads stay in bounds
+  const uint16_t* src = a.k + ((size_t)hk * a.Nk + j) * kD;
+  uint16_t* dst = a.k_rot + ((size_t)hk * a.Nk + j) * kD;
+  uint4 lo, hi;
+  rotate_chunks(*reinterpret_cast<const uint4*>(src + 8 * c), *reinterpret_cast<const uint4*>(src + kHalf + 8 * c),
+                a.rope_cos + (size_t)pc * kHalf + 8 * c, a.rope_sin + (size_t)pc * kHalf + 8 * c, lo, hi);
+  *reinterpret_cast<uint4*>(dst + 8 * c) = lo;
+  *reinterpret_cast<uint4*>(dst + kHalf + 8 * c) = hi;
 }
 
 // Per-tile minimum key positions kept for the skip test (tiles beyond this
@@ -161,7 +183,8 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
   float m = -INFINITY, lsum = 0.0f;
   const float sl2 = a.scale_log2e;
 
-  const __amdgpu_buffer_rsrc_t kres = make_rsrc(a.k + (size_t)hk * a.Nk * kD, (uint32_t)((size_t)a.Nk * kD * 2));
+  const __amdgpu_buffer_rsrc_t kres =
+      make_rsrc(a.k_rot + (size_t)hk * a.Nk * kD, (uint32_t)((size_t)a.Nk * kD * 2));
   const __amdgpu_buffer_rsrc_t vres = make_rsrc(a.v + (size_t)hk * a.Nk * kD, (uint32_t)((size_t)a.Nk * kD * 2));
   // staging: for the keys, thread tid handles key tid / 8 of the tile and
   // the pair of 8-element chunks (8 c, 64 + 8 c), c = tid % 8; for the
@@ -171,7 +194,6 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
   const int sj = tid >> 3, sc = tid & 7;
   const int vkp = tid & 15, vc = tid >> 4;
   uint4 gk0, gk1, gv0, gv1;
-  float gcs[8], gsn[8];
   int gpj;
   auto load_tile = [&](int t) {
     const int j = t * kKeys + sj;
@@ -183,18 +205,10 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
     gk1 = buf_load16(kres, ko == kOOB ? kOOB : ko + kHalf * 2);
     gv0 = buf_load16(vres, jv0 < a.Nk ? (uint32_t)((jv0 * kD + 8 * vc) * 2) : kOOB);
     gv1 = buf_load16(vres, jv1 < a.Nk ? (uint32_t)((jv1 * kD + 8 * vc) * 2) : kOOB);
-    const int pc = clamp_pos(ok ? gpj : 0);
-    const float4* cp = reinterpret_cast<const float4*>(a.rope_cos + (size_t)pc * kHalf + 8 * sc);
-    const float4* sp = reinterpret_cast<const float4*>(a.rope_sin + (size_t)pc * kHalf + 8 * sc);
-    const float4 c0 = cp[0], c1 = cp[1], s0 = sp[0], s1 = sp[1];
-    gcs[0] = c0.x; gcs[1] = c0.y; gcs[2] = c0.z; gcs[3] = c0.w; gcs[4] = c1.x; gcs[5] = c1.y; gcs[6] = c1.z; gcs[7] = c1.w;
-    gsn[0] = s0.x; gsn[1] = s0.y; gsn[2] = s0.z; gsn[3] = s0.w; gsn[4] = s1.x; gsn[5] = s1.y; gsn[6] = s1.z; gsn[7] = s1.w;
   };
   auto store_tile = [&](int b) {
-    uint4 lo, hi;
-    rotate_chunks(gk0, gk1, gcs, gsn, lo, hi);
-    *reinterpret_cast<uint4*>(&l_k[b][sj * kKPitch + 8 * sc]) = lo;
-    *reinterpret_cast<uint4*>(&l_k[b][sj * kKPitch + kHalf + 8 * sc]) = hi;
+    *reinterpret_cast<uint4*>(&l_k[b][sj * kKPitch + 8 * sc]) = gk0;
+    *reinterpret_cast<uint4*>(&l_k[b][sj * kKPitch + kHalf + 8 * sc]) = gk1;
     // row d of the transposed tile gets (v[2 kp][d], v[2 kp + 1][d]) as one dword
     const uint32_t w0[4] = {gv0.x, gv0.y, gv0.z, gv0.w}, w1[4] = {gv1.x, gv1.y, gv1.z, gv1.w};
 #pragma unroll
@@ -352,12 +366,13 @@ int stream_attention_splits(int H, int Nq, int Nk) {
   return S;
 }
 
-// Workspace: the partials, past the counter region shared with the linear
-// calls' workspaces (left untouched here).
+// Workspace, past the counter region shared with the linear calls'
+// workspaces (left untouched here): the rotated keys (room for H kv heads,
+// the most a call with H query heads has), then the split partials.
+size_t rotated_keys_bytes(int H, int Nk) { return ((size_t)H * Nk * kD * 2 + 255) / 256 * 256; }
 size_t stream_attention_workspace(int H, int Nq, int Nk) {
   const int S = stream_attention_splits(H, Nq, Nk);
-  if (S == 1) return 0;
-  return kCounterRegionBytes + (size_t)S * H * Nq * (kD + 2) * sizeof(float);
+  return kCounterRegionBytes + rotated_keys_bytes(H, Nk) + (S > 1 ? (size_t)S * H * Nq * (kD + 2) * sizeof(float) : 0);
 }
 
 hipError_t launch_stream_attention(const AttnArgs& a0, hipStream_t stream) {
@@ -367,10 +382,13 @@ hipError_t launch_stream_attention(const AttnArgs& a0, hipStream_t stream) {
   a.S = stream_attention_splits(a.H, a.Nq, a.Nk);
   a.tiles_per_split = (ntiles + a.S - 1) / a.S;
   a.S = (ntiles + a.tiles_per_split - 1) / a.tiles_per_split;  // no empty trailing split
+  uint8_t* ws = static_cast<uint8_t*>(a.workspace) + kCounterRegionBytes;
+  a.k_rot = reinterpret_cast<uint16_t*>(ws);
   if (a.S > 1) {
-    a.part_o = reinterpret_cast<float*>(static_cast<uint8_t*>(a.workspace) + kCounterRegionBytes);
+    a.part_o = reinterpret_cast<float*>(ws + rotated_keys_bytes(a.H, a.Nk));
     a.part_ml = a.part_o + (size_t)a.S * a.H * a.Nq * kD;
   }
+  rotate_keys<<<dim3((unsigned)ntiles, (unsigned)a.Hkv), dim3(256), 0, stream>>>(a);
   const dim3 grid((unsigned)((a.Nq + kQPerBlock - 1) / kQPerBlock), (unsigned)a.H, (unsigned)a.S);
   stream_attention<<<grid, dim3(kAttnWaves * 64), 0, stream>>>(a);
   if (a.S > 1) {

@@ -105,8 +105,9 @@ struct AttnArgs {
   uint16_t* o;            // bf16 [H][Nq][128]
   int H, Hkv, Nq, Nk, n_pos;
   float scale_log2e;      // score scale times log2(e)
-  void* workspace;        // split partial results (stream_attention_workspace bytes)
+  void* workspace;        // rotated keys and split partials (stream_attention_workspace bytes)
   // set by the launcher
+  uint16_t* k_rot;        // bf16 [Hkv][Nk][128]: the keys rotated at their positions
   int S, tiles_per_split;
   float* part_o;          // [S][H][Nq][128] unnormalized partial sums
   float* part_ml;         // [S][H][Nq][2] running maximum (base 2) and weight total

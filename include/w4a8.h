@@ -186,8 +186,9 @@ w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, 
  *   workspace    device, >= w4a8_stream_attention_workspace_bytes(H, Nq, Nk)
  *                bytes, 256-byte aligned: the keys rotated at their
  *                positions (computed once per call, read by every query
- *                head of their kv head) and the partial results of
- *                key-range splits, all written before read (no zero fill
+ *                head of their kv head), each 32-key tile's smallest and
+ *                largest position, and the partial results of key-range
+ *                splits, all written before read (no zero fill
  *                needed), past the first 64 KiB, which this call leaves
  *                untouched, so that it may share one buffer with
  *                w4a8_linear's workspace; concurrent calls must not share it

@@ -11,19 +11,25 @@
 // view-major order of the window.
 //
 // A first kernel rotates the window's keys once per call, at the
-// positions they occupy now (every query head of a kv head reads them).
-// Then one workgroup per (64 queries, head); each of its 4 waves owns 16
-// queries.  Key tiles that none of its queries can see are skipped.  Per
-// 32-key tile:
+// positions they occupy now (every query head of a kv head reads them), and
+// records each 32-key tile's smallest and largest position.  Then one
+// workgroup per (64 queries, head, key split); each of its 4 waves owns 16
+// queries.  Key tiles that none of its queries can see are skipped, and a
+// split none of them sees ends the workgroup before its queries are
+// rotated.  Per 32-key tile:
 //   - the workgroup stages the rotated keys (bf16, [key][d]) and the values
 //     transposed ([d][key]) in LDS;
 //   - a wave forms S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (its rotated
 //     queries are the B operand, held in registers), so a lane holds one
 //     query's scores for 8 keys;
-//   - online softmax in fp32 (base-2 exponentials, the scale folded into
-//     log2 e), the weights rounded to bf16 as the B operand of O^T += V^T P^T;
-//     the 8 keys a lane holds are the reduction indices of its lane group,
-//     and V^T is read from LDS in the same key order.
+//   - online softmax in fp32: base-2 hardware exponentials of
+//     score * (scale log2 e) - running maximum as one fused multiply-add
+//     (weights below 2^-126 of the largest may flush to 0), the per-score
+//     position test only on tiles that straddle a query of the wave, and
+//     row swaps across the lane groups of a query;
+//   - the weights rounded to bf16 as the B operand of O^T += V^T P^T; the 8
+//     keys a lane holds are the reduction indices of its lane group, and V^T
+//     is read from LDS in the same key order.
 // Rotations are fp32 IEEE operations rounded to bf16, as a bf16 model holds
 // its rotated operands.
 #include <climits>
@@ -51,6 +57,20 @@ constexpr int kKPitch = kD + 8;
 constexpr int kVtPitch = kKeys + 4;
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8_t, u); }
+
+// Reductions over the lane pairs (l, l ^ 16) and (l, l ^ 32) with the gfx950
+// row swaps (no LDS round trip): each swap hands a lane its partner's value
+// in one of the two results and its own in the other.  Scores are never NaN.
+__device__ __forceinline__ float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
+  return a > b ? a : b;
+}
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
+  return a > b ? a : b;
+}
 
 // The rotated pair chunks (8 values each at d and d + 64) of one row at
 // position pos, as bf16 words: lo = a cos - b sin, hi = b cos + a sin.
@@ -82,6 +102,19 @@ __device__ __forceinline__ void rotate_chunks(uint4 a8, uint4 b8, const float* c
 // the kv head's query heads) took 21 us off the bench workload's 114 us.
 __global__ __launch_bounds__(256) void rotate_keys(const AttnArgs a) {
   const int tid = threadIdx.x, hk = blockIdx.y;
+  if (hk == 0 && tid < 64) {
+    // the tile's smallest and largest key positions (keys past Nk count as
+    // unseen), read by every workgroup of the attention for its skip and
+    // mask tests
+    const int jj = blockIdx.x * kKeys + (tid & (kKeys - 1));
+    int mn = jj < a.Nk ? a.pos_k[jj] : INT_MAX, mx = mn;
+#pragma unroll
+    for (int off = kKeys / 2; off >= 1; off >>= 1) {
+      mn = min(mn, __shfl_xor(mn, off, 64));
+      mx = max(mx, __shfl_xor(mx, off, 64));
+    }
+    if (tid == 0) a.tile_bounds[blockIdx.x] = make_int2(mn, mx);
+  }
   const int j = blockIdx.x * kKeys + (tid >> 3), c = tid & 7;
   if (j >= a.Nk) return;
   const int P = a.n_pos, p = a.pos_k[j];
@@ -100,8 +133,8 @@ __global__ __launch_bounds__(256) void rotate_keys(const AttnArgs a) {
 constexpr int kMaxSkipTiles = 512;
 
 // The occupancy hint (4 workgroups, i.e. 4 waves per SIMD) holds the kernel
-// to 128 registers; the few it spills are prologue values reloaded after the
-// key loop, which runs without scratch traffic.
+// to 128 registers (it needs 110, without spills); LDS (39.3 KiB per
+// workgroup) also fits 4.
 __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const AttnArgs a) {
   // two stages of the key / value tile: the next visible tile is staged
   // while the current one is computed
@@ -109,6 +142,7 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
   __shared__ __align__(16) uint16_t l_vt[2][kD * kVtPitch];      // values transposed [d][key]
   __shared__ int l_pos[2][kKeys];
   __shared__ int l_tmin[kMaxSkipTiles];
+  __shared__ int l_tmax[kMaxSkipTiles];
   __shared__ int l_qmax[kAttnWaves];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -129,19 +163,14 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
   // read zeros (selects of a loaded value against a zero vector had put the
   // zero in scratch memory, on the loop's critical path).
   const __amdgpu_buffer_rsrc_t qres = make_rsrc(a.q + (size_t)h * a.Nq * kD, (uint32_t)((size_t)a.Nq * kD * 2));
-  bf16x8_t qf[4];
+  uint4 qraw[2][2];  // chunks (32 i + 8 g, + 64), rotated once the block is known to see a key
   {
     const uint32_t qoff = q_ok ? (uint32_t)(qi * kD * 2) : kOOB;
-    const int pc = clamp_pos(q_ok ? pq : 0);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int d = 32 * i + 8 * g;  // < 64
-      const uint4 x0 = buf_load16(qres, qoff == kOOB ? kOOB : qoff + d * 2);
-      const uint4 x1 = buf_load16(qres, qoff == kOOB ? kOOB : qoff + (d + kHalf) * 2);
-      uint4 lo, hi;
-      rotate_chunks(x0, x1, a.rope_cos + (size_t)pc * kHalf + d, a.rope_sin + (size_t)pc * kHalf + d, lo, hi);
-      qf[i] = as_bf16x8(lo);
-      qf[i + 2] = as_bf16x8(hi);
+      qraw[i][0] = buf_load16(qres, qoff == kOOB ? kOOB : qoff + d * 2);
+      qraw[i][1] = buf_load16(qres, qoff == kOOB ? kOOB : qoff + (d + kHalf) * 2);
     }
   }
 
@@ -152,19 +181,22 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
   const int t_begin = split * a.tiles_per_split;
   const int ntiles = min(ntiles_all, t_begin + a.tiles_per_split);  // one past the last tile
   const bool skipping = ntiles - t_begin <= kMaxSkipTiles;
+  int wave_qmin;  // the wave's smallest query position (INT_MAX when it has no query)
   {
-    int qm = pq;
+    int qm = pq, qn = q_ok ? pq : INT_MAX;
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) qm = max(qm, __shfl_xor(qm, off, 64));
+    for (int off = 32; off >= 1; off >>= 1) {
+      qm = max(qm, __shfl_xor(qm, off, 64));
+      qn = min(qn, __shfl_xor(qn, off, 64));
+    }
     if (lane == 0) l_qmax[wave] = qm;
-    // 32 threads per tile (one key each), 8 tiles per pass
+    wave_qmin = __builtin_amdgcn_readfirstlane(qn);
+    // the split's tile bounds, one tile per thread
     if (skipping)
-      for (int t0 = t_begin; t0 < ntiles; t0 += kAttnWaves * 64 / kKeys) {
-        const int t = t0 + tid / kKeys, j = t * kKeys + tid % kKeys;
-        int mn = t < ntiles && j < a.Nk ? a.pos_k[j] : INT_MAX;
-#pragma unroll
-        for (int off = kKeys / 2; off >= 1; off >>= 1) mn = min(mn, __shfl_xor(mn, off, 64));
-        if (tid % kKeys == 0 && t < ntiles) l_tmin[t - t_begin] = mn;
+      for (int t = t_begin + tid; t < ntiles; t += kAttnWaves * 64) {
+        const int2 bd = a.tile_bounds[t];
+        l_tmin[t - t_begin] = bd.x;
+        l_tmax[t - t_begin] = bd.y;
       }
   }
   __syncthreads();
@@ -176,6 +208,28 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
       while (t < ntiles && l_tmin[t - t_begin] > wg_qmax) ++t;
     return t;
   };
+  int cur = next_visible(t_begin);
+  if (a.S > 1 && cur >= ntiles) {
+    // no query of the block sees a key of this split: an empty partial
+    // (the merge reads only its maximum)
+    if (q_ok && g == 0)
+      *reinterpret_cast<float2*>(a.part_ml + (((size_t)split * a.H + h) * a.Nq + qi) * 2) = make_float2(-INFINITY, 0.0f);
+    return;
+  }
+
+  bf16x8_t qf[4];
+  {
+    const int pc = clamp_pos(q_ok ? pq : 0);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int d = 32 * i + 8 * g;
+      uint4 lo, hi;
+      rotate_chunks(qraw[i][0], qraw[i][1], a.rope_cos + (size_t)pc * kHalf + d, a.rope_sin + (size_t)pc * kHalf + d,
+                    lo, hi);
+      qf[i] = as_bf16x8(lo);
+      qf[i + 2] = as_bf16x8(hi);
+    }
+  }
 
   f32x4_t acc[kD / 16];
 #pragma unroll
@@ -221,9 +275,13 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
     if (sc == 0) l_pos[b][sj] = gpj;
   };
 
-  auto compute_tile = [&](int b) {
+  auto compute_tile = [&](int b, int t) {
     // ---- S^T for keys 16 u + (4 g + r), u = 0, 1: lane holds query r16
+    // (raw scores; the scale is applied inside the exponent)
     float s[2][4];
+    // the position test per score only where some key of the tile lies
+    // beyond some query of the wave
+    const bool full = skipping && l_tmax[t - t_begin] <= wave_qmin;
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       f32x4_t c = {0.f, 0.f, 0.f, 0.f};
@@ -233,28 +291,35 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
         c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[i], c, 0, 0, 0);
       }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool vis = l_pos[b][16 * u + 4 * g + r] <= pq;
-        s[u][r] = vis ? c[r] * sl2 : -INFINITY;
-      }
+      for (int r = 0; r < 4; ++r) s[u][r] = c[r];
+    }
+    if (!full) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (l_pos[b][16 * u + 4 * g + r] > pq) s[u][r] = -INFINITY;
     }
     // ---- online softmax over this lane's query (its 8 keys here, then the
-    // 4 lane groups holding the same query)
+    // 4 lane groups holding the same query), in scaled base-2 units: the
+    // scale is positive, so the largest raw score gives the largest scaled one
     float tmax = -INFINITY;
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, s[u][r]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    tmax = max_xor32(max_xor16(tmax)) * sl2;
     const float mnew = fmaxf(m, tmax);
-    const float alpha = mnew == m ? 1.0f : exp2f(m - mnew);  // also 1 while nothing is visible yet
+    // exponent offset: while nothing is visible yet the masked scores
+    // (-inf) must still give 0
+    const float mb = mnew == -INFINITY ? 0.0f : mnew;
+    const float alpha = __builtin_amdgcn_exp2f(m - mb);  // 0 while m is -inf (the sums are 0 then)
     float p[2][4], psum = 0.0f;
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        p[u][r] = s[u][r] == -INFINITY ? 0.0f : exp2f(s[u][r] - mnew);
+        p[u][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[u][r], sl2, -mb));
         psum += p[u][r];
       }
     lsum = lsum * alpha + psum;
@@ -279,7 +344,6 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
 
   // One barrier per tile: stage b is computed while stage b ^ 1 is filled;
   // stage b ^ 1 was last read before the previous barrier.
-  int cur = next_visible(t_begin);
   if (cur < ntiles) {
     load_tile(cur);
     store_tile(0);
@@ -289,7 +353,7 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
   while (cur < ntiles) {
     const int nxt = next_visible(cur + 1);
     if (nxt < ntiles) load_tile(nxt);
-    compute_tile(b);
+    compute_tile(b, cur);
     if (nxt < ntiles) store_tile(b ^ 1);
     __syncthreads();
     b ^= 1;
@@ -305,9 +369,10 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
     // (base 2, scaled scores) and weight total; attn_combine merges them
     const size_t row = ((size_t)split * a.H + h) * a.Nq + qi;
     float* po = a.part_o + row * kD;
+    if (m != -INFINITY)  // the merge reads no sum of a split that saw nothing
 #pragma unroll
-    for (int t = 0; t < kD / 16; ++t)
-      *reinterpret_cast<float4*>(po + 16 * t + 4 * g) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+      for (int t = 0; t < kD / 16; ++t)
+        *reinterpret_cast<float4*>(po + 16 * t + 4 * g) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
     if (g == 0) *reinterpret_cast<float2*>(a.part_ml + row * 2) = make_float2(m, lsum);
     return;
   }
@@ -370,9 +435,11 @@ int stream_attention_splits(int H, int Nq, int Nk) {
 // workspaces (left untouched here): the rotated keys (room for H kv heads,
 // the most a call with H query heads has), then the split partials.
 size_t rotated_keys_bytes(int H, int Nk) { return ((size_t)H * Nk * kD * 2 + 255) / 256 * 256; }
+size_t tile_bounds_bytes(int Nk) { return ((size_t)(Nk + kKeys - 1) / kKeys * sizeof(int2) + 255) / 256 * 256; }
 size_t stream_attention_workspace(int H, int Nq, int Nk) {
   const int S = stream_attention_splits(H, Nq, Nk);
-  return kCounterRegionBytes + rotated_keys_bytes(H, Nk) + (S > 1 ? (size_t)S * H * Nq * (kD + 2) * sizeof(float) : 0);
+  return kCounterRegionBytes + rotated_keys_bytes(H, Nk) + tile_bounds_bytes(Nk) +
+         (S > 1 ? (size_t)S * H * Nq * (kD + 2) * sizeof(float) : 0);
 }
 
 hipError_t launch_stream_attention(const AttnArgs& a0, hipStream_t stream) {
@@ -384,8 +451,9 @@ hipError_t launch_stream_attention(const AttnArgs& a0, hipStream_t stream) {
   a.S = (ntiles + a.tiles_per_split - 1) / a.tiles_per_split;  // no empty trailing split
   uint8_t* ws = static_cast<uint8_t*>(a.workspace) + kCounterRegionBytes;
   a.k_rot = reinterpret_cast<uint16_t*>(ws);
+  a.tile_bounds = reinterpret_cast<int2*>(ws + rotated_keys_bytes(a.H, a.Nk));
   if (a.S > 1) {
-    a.part_o = reinterpret_cast<float*>(ws + rotated_keys_bytes(a.H, a.Nk));
+    a.part_o = reinterpret_cast<float*>(ws + rotated_keys_bytes(a.H, a.Nk) + tile_bounds_bytes(a.Nk));
     a.part_ml = a.part_o + (size_t)a.S * a.H * a.Nq * kD;
   }
   rotate_keys<<<dim3((unsigned)ntiles, (unsigned)a.Hkv), dim3(256), 0, stream>>>(a);

@@ -108,6 +108,7 @@ struct AttnArgs {
   void* workspace;        // rotated keys and split partials (stream_attention_workspace bytes)
   // set by the launcher
   uint16_t* k_rot;        // bf16 [Hkv][Nk][128]: the keys rotated at their positions
+  int2* tile_bounds;      // [ceil(Nk / 32)] smallest and largest key position of each 32-key tile
   int S, tiles_per_split;
   float* part_o;          // [S][H][Nq][128] unnormalized partial sums
   float* part_ml;         // [S][H][Nq][2] running maximum (base 2) and weight total

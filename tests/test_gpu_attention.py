@@ -124,7 +124,8 @@ def test_long_cache_without_tile_skipping():
     H, Hkv, Nq, Nk = 8, 2, len(pos_q), len(pos_k)
     # workspace: 64 KiB, the rotated keys (H * Nk * 128 bf16), the partials
     rot = (H * Nk * 128 * 2 + 255) // 256 * 256
-    S = (w.w4a8_stream_attention_workspace_bytes(H, Nq, Nk) - 64 * 1024 - rot) // (H * Nq * 130 * 4)
+    bounds = ((Nk + 31) // 32 * 8 + 255) // 256 * 256
+    S = (w.w4a8_stream_attention_workspace_bytes(H, Nq, Nk) - 64 * 1024 - rot - bounds) // (H * Nq * 130 * 4)
     assert S >= 1 and (Nk // 32) / S > 512
     rows = np.sort(np.random.Generator(np.random.PCG64(809)).choice(Nq, 64, replace=False))
     check(H, Hkv, pos_q, pos_k, 810, "long cache 1x10x4096", rows=rows)

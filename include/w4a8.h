@@ -187,7 +187,8 @@ w4a8_status w4a8_rmsnorm_quantize_act(const uint16_t* x, const uint16_t* gamma, 
  *                bytes, 256-byte aligned: the keys rotated at their
  *                positions (computed once per call, read by every query
  *                head of their kv head), each 32-key tile's smallest and
- *                largest position, and the partial results of key-range
+ *                largest position, the order in which workgroups take the
+ *                work items, and the partial results of key-range
  *                splits, all written before read (no zero fill
  *                needed), past the first 64 KiB, which this call leaves
  *                untouched, so that it may share one buffer with

@@ -11,12 +11,14 @@
 // view-major order of the window.
 //
 // A first kernel rotates the window's keys once per call, at the
-// positions they occupy now (every query head of a kv head reads them), and
-// records each 32-key tile's smallest and largest position.  Then one
-// workgroup per (64 queries, head, key split); each of its 4 waves owns 16
-// queries.  Key tiles that none of its queries can see are skipped, and a
-// split none of them sees ends the workgroup before its queries are
-// rotated.  Per 32-key tile:
+// positions they occupy now (every query head of a kv head reads them),
+// records each 32-key tile's smallest and largest position, and (one more
+// workgroup) deals the attention's work items to workgroup ids so that the
+// CUs get even shares: a query block late in the window sees many more key
+// tiles than an early one.  Then one workgroup per (64 queries, head, key
+// split); each of its 4 waves owns 16 queries.  Key tiles that none of its
+// queries can see are skipped, and a split none of them sees ends the
+// workgroup before its queries are rotated.  Per 32-key tile:
 //   - the workgroup stages the rotated keys (bf16, [key][d]) and the values
 //     transposed ([d][key]) in LDS;
 //   - a wave forms S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (its rotated
@@ -100,8 +102,90 @@ __device__ __forceinline__ void rotate_chunks(uint4 a8, uint4 b8, const float* c
 // thread, 32 keys of one kv head per workgroup.  Rotating each key once
 // here instead of in every workgroup that stages it (all query blocks of
 // the kv head's query heads) took 21 us off the bench workload's 114 us.
+// Limits of the dispatch schedule (larger calls keep the plain order).
+constexpr int kSchedMaxClasses = 256;  // (query block, split) pairs
+constexpr int kRotHeads = 2;  // kv heads per thread of the key rotation
+constexpr int kSchedMaxTiles = 1024;   // 32-key tiles
+
+// The order in which the attention's workgroups take their work items.
+// Workgroup ids are dealt to the CUs in rounds of C consecutive ids (id mod
+// C picks the CU while every workgroup is resident), so a CU runs one item
+// of each round side by side.  The items are ranked by their number of
+// visible key tiles (the same for every head of a (query block, split)
+// pair) and dealt heaviest first, every second round in reverse: a CU that
+// gets one of the heaviest items of a round gets one of the lightest of the
+// next.  sched[id] = (query block * S + split) * H + head.
+__device__ void build_schedule(const AttnArgs& a) {
+  __shared__ int s_qmax[kSchedMaxClasses];
+  __shared__ int s_tmin[kSchedMaxTiles];
+  __shared__ int s_vis[kSchedMaxClasses];
+  __shared__ int s_class_of_rank[kSchedMaxClasses];
+  const int tid = threadIdx.x;
+  const int X = (a.Nq + kQPerBlock - 1) / kQPerBlock, ntiles = (a.Nk + kKeys - 1) / kKeys;
+  const int S = a.S, n = X * S, H = a.H;
+  // each block's largest query position and each tile's smallest key
+  // position: every thread sweeps the position arrays with independent
+  // loads and folds them into LDS with atomics
+  for (int x = tid; x < X; x += 256) s_qmax[x] = INT_MIN;
+  for (int t = tid; t < ntiles; t += 256) s_tmin[t] = INT_MAX;
+  __syncthreads();
+  // both position arrays swept together, so that every thread's loads of
+  // both go out before any of its atomics
+  constexpr int kBatch = 16;  // loads in flight per array and thread
+  const int span = max(a.Nq, a.Nk);
+  for (int i0 = tid; i0 < span; i0 += 256 * kBatch) {
+    int vq[kBatch], vk[kBatch];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int i = i0 + 256 * b;
+      vq[b] = i < a.Nq ? a.pos_q[i] : INT_MIN;
+      vk[b] = i < a.Nk ? a.pos_k[i] : INT_MAX;
+    }
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int i = i0 + 256 * b;
+      if (i < a.Nq) atomicMax(&s_qmax[i / kQPerBlock], vq[b]);
+      if (i < a.Nk) atomicMin(&s_tmin[i / kKeys], vk[b]);
+    }
+  }
+  for (int c = tid; c < n; c += 256) s_vis[c] = 0;
+  __syncthreads();
+  // visible tiles of each (block, split) class, one (class, tile) pair per
+  // thread and step (the counter a lane adds to depends on its index)
+  const int tps = a.tiles_per_split;
+  for (int i = tid; i < n * tps; i += 256) {
+    const int c = i / tps, t = (c % S) * tps + (i - c * tps);
+    if (t < ntiles && s_tmin[t] <= s_qmax[c / S]) atomicAdd(&s_vis[c], 1);
+  }
+  __syncthreads();
+  // rank of each class: heavier first, ties in class order
+  for (int c = tid; c < n; c += 256) {
+    const int vc = s_vis[c];
+    int r = 0;
+#pragma unroll 8
+    for (int c2 = 0; c2 < n; ++c2) {
+      const int v2 = s_vis[c2];
+      r += (v2 > vc || (v2 == vc && c2 < c)) ? 1 : 0;
+    }
+    s_class_of_rank[r] = c;
+  }
+  __syncthreads();
+  // item k of the ranked list is class s_class_of_rank[k / H], head k % H
+  const int G = n * H, C = a.sched_cus;
+  for (int k = tid; k < G; k += 256) {
+    const int r = k / H, h = k - r * H;
+    const int round = k / C, p = k - round * C;
+    const bool reversed = (round & 1) && (round + 1) * C <= G;  // a partial last round keeps its order
+    a.sched[round * C + (reversed ? C - 1 - p : p)] = s_class_of_rank[r] * H + h;
+  }
+}
+
 __global__ __launch_bounds__(256) void rotate_keys(const AttnArgs a) {
   const int tid = threadIdx.x, hk = blockIdx.y;
+  if ((int)blockIdx.x * kKeys >= a.Nk) {  // the column past the last tile: the schedule
+    if (hk == 0) build_schedule(a);
+    return;
+  }
   if (hk == 0 && tid < 64) {
     // the tile's smallest and largest key positions (keys past Nk count as
     // unseen), read by every workgroup of the attention for its skip and
@@ -119,13 +203,33 @@ __global__ __launch_bounds__(256) void rotate_keys(const AttnArgs a) {
   if (j >= a.Nk) return;
   const int P = a.n_pos, p = a.pos_k[j];
   const int pc = p < 0 ? 0 : (p >= P ? P - 1 : p);  // table reads stay in bounds
-  const uint16_t* src = a.k + ((size_t)hk * a.Nk + j) * kD;
-  uint16_t* dst = a.k_rot + ((size_t)hk * a.Nk + j) * kD;
-  uint4 lo, hi;
-  rotate_chunks(*reinterpret_cast<const uint4*>(src + 8 * c), *reinterpret_cast<const uint4*>(src + kHalf + 8 * c),
-                a.rope_cos + (size_t)pc * kHalf + 8 * c, a.rope_sin + (size_t)pc * kHalf + 8 * c, lo, hi);
-  *reinterpret_cast<uint4*>(dst + 8 * c) = lo;
-  *reinterpret_cast<uint4*>(dst + kHalf + 8 * c) = hi;
+  // kRotHeads kv heads per thread share one read of the table row
+  const int h0 = hk * kRotHeads, nh = min(kRotHeads, a.Hkv - h0);
+  uint4 x0[kRotHeads], x1[kRotHeads];
+#pragma unroll
+  for (int i = 0; i < kRotHeads; ++i)
+    if (i < nh) {
+      const uint16_t* src = a.k + ((size_t)(h0 + i) * a.Nk + j) * kD;
+      x0[i] = *reinterpret_cast<const uint4*>(src + 8 * c);
+      x1[i] = *reinterpret_cast<const uint4*>(src + kHalf + 8 * c);
+    }
+  float cs[8], sn[8];
+  {
+    const float4* cp = reinterpret_cast<const float4*>(a.rope_cos + (size_t)pc * kHalf + 8 * c);
+    const float4* sp = reinterpret_cast<const float4*>(a.rope_sin + (size_t)pc * kHalf + 8 * c);
+    const float4 c0 = cp[0], c1 = cp[1], s0 = sp[0], s1 = sp[1];
+    cs[0] = c0.x; cs[1] = c0.y; cs[2] = c0.z; cs[3] = c0.w; cs[4] = c1.x; cs[5] = c1.y; cs[6] = c1.z; cs[7] = c1.w;
+    sn[0] = s0.x; sn[1] = s0.y; sn[2] = s0.z; sn[3] = s0.w; sn[4] = s1.x; sn[5] = s1.y; sn[6] = s1.z; sn[7] = s1.w;
+  }
+#pragma unroll
+  for (int i = 0; i < kRotHeads; ++i)
+    if (i < nh) {
+      uint4 lo, hi;
+      rotate_chunks(x0[i], x1[i], cs, sn, lo, hi);
+      uint16_t* dst = a.k_rot + ((size_t)(h0 + i) * a.Nk + j) * kD;
+      *reinterpret_cast<uint4*>(dst + 8 * c) = lo;
+      *reinterpret_cast<uint4*>(dst + kHalf + 8 * c) = hi;
+    }
 }
 
 // Per-tile minimum key positions kept for the skip test (tiles beyond this
@@ -147,8 +251,14 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int h = blockIdx.y, hk = h / (a.H / a.Hkv);
-  const int split = blockIdx.z;
+  int xb = blockIdx.x, h = blockIdx.y, split = blockIdx.z;  // this workgroup's item
+  if (a.sched) {  // a 1-D grid dealt by the schedule
+    const int code = a.sched[blockIdx.x], c = code / a.H;
+    h = code % a.H;
+    xb = c / a.S;
+    split = c % a.S;
+  }
+  const int hk = h / (a.H / a.Hkv);
   const int r16 = lane & 15, g = lane >> 4;
   const int P = a.n_pos;
   auto clamp_pos = [&](int p) { return p < 0 ? 0 : (p >= P ? P - 1 : p); };  // table reads stay in bounds
@@ -156,7 +266,7 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
   // ---- this lane's query: rotated, as the B operand of S^T = K Q^T
   // (lane: query r16, d chunk 32 i + 8 g for MFMA i; chunks i and i + 2 are
   // a rotate-half pair)
-  const int qi = blockIdx.x * kQPerBlock + wave * kQPerWave + r16;
+  const int qi = xb * kQPerBlock + wave * kQPerWave + r16;
   const bool q_ok = qi < a.Nq;
   const int pq = q_ok ? a.pos_q[qi] : INT_MIN;
   // Rows past Nq and keys past Nk are out-of-range buffer offsets, which
@@ -436,28 +546,59 @@ int stream_attention_splits(int H, int Nq, int Nk) {
 // the most a call with H query heads has), then the split partials.
 size_t rotated_keys_bytes(int H, int Nk) { return ((size_t)H * Nk * kD * 2 + 255) / 256 * 256; }
 size_t tile_bounds_bytes(int Nk) { return ((size_t)(Nk + kKeys - 1) / kKeys * sizeof(int2) + 255) / 256 * 256; }
+// The splits a call uses (the split rule, without empty trailing splits).
+int used_splits(int H, int Nq, int Nk, int* tiles_per_split) {
+  const int ntiles = (Nk + kKeys - 1) / kKeys;
+  const int S = stream_attention_splits(H, Nq, Nk);
+  const int tps = (ntiles + S - 1) / S;
+  if (tiles_per_split) *tiles_per_split = tps;
+  return (ntiles + tps - 1) / tps;
+}
+// Bytes of the dispatch schedule (0 for calls past its limits).
+size_t schedule_bytes(int H, int Nq, int Nk) {
+  const long classes = (long)((Nq + kQPerBlock - 1) / kQPerBlock) * used_splits(H, Nq, Nk, nullptr);
+  if (classes > kSchedMaxClasses || (Nk + kKeys - 1) / kKeys > kSchedMaxTiles) return 0;
+  return ((size_t)classes * H * sizeof(int) + 255) / 256 * 256;
+}
 size_t stream_attention_workspace(int H, int Nq, int Nk) {
   const int S = stream_attention_splits(H, Nq, Nk);
-  return kCounterRegionBytes + rotated_keys_bytes(H, Nk) + tile_bounds_bytes(Nk) +
+  return kCounterRegionBytes + rotated_keys_bytes(H, Nk) + tile_bounds_bytes(Nk) + schedule_bytes(H, Nq, Nk) +
          (S > 1 ? (size_t)S * H * Nq * (kD + 2) * sizeof(float) : 0);
+}
+
+// Compute units of the current device (looked up once per device).
+int compute_units() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
 }
 
 hipError_t launch_stream_attention(const AttnArgs& a0, hipStream_t stream) {
   if (a0.Nq == 0) return hipSuccess;
   AttnArgs a = a0;
   const int ntiles = (a.Nk + kKeys - 1) / kKeys;
-  a.S = stream_attention_splits(a.H, a.Nq, a.Nk);
-  a.tiles_per_split = (ntiles + a.S - 1) / a.S;
-  a.S = (ntiles + a.tiles_per_split - 1) / a.tiles_per_split;  // no empty trailing split
+  a.S = used_splits(a.H, a.Nq, a.Nk, &a.tiles_per_split);
   uint8_t* ws = static_cast<uint8_t*>(a.workspace) + kCounterRegionBytes;
   a.k_rot = reinterpret_cast<uint16_t*>(ws);
   a.tile_bounds = reinterpret_cast<int2*>(ws + rotated_keys_bytes(a.H, a.Nk));
+  const size_t sched_bytes = schedule_bytes(a.H, a.Nq, a.Nk);
+  a.sched = sched_bytes ? reinterpret_cast<int*>(ws + rotated_keys_bytes(a.H, a.Nk) + tile_bounds_bytes(a.Nk)) : nullptr;
+  a.sched_cus = compute_units();
   if (a.S > 1) {
-    a.part_o = reinterpret_cast<float*>(ws + rotated_keys_bytes(a.H, a.Nk) + tile_bounds_bytes(a.Nk));
+    a.part_o = reinterpret_cast<float*>(ws + rotated_keys_bytes(a.H, a.Nk) + tile_bounds_bytes(a.Nk) + sched_bytes);
     a.part_ml = a.part_o + (size_t)a.S * a.H * a.Nq * kD;
   }
-  rotate_keys<<<dim3((unsigned)ntiles, (unsigned)a.Hkv), dim3(256), 0, stream>>>(a);
-  const dim3 grid((unsigned)((a.Nq + kQPerBlock - 1) / kQPerBlock), (unsigned)a.H, (unsigned)a.S);
+  rotate_keys<<<dim3((unsigned)(ntiles + (a.sched ? 1 : 0)), (unsigned)((a.Hkv + kRotHeads - 1) / kRotHeads)), dim3(256), 0,
+                stream>>>(a);
+  const unsigned X = (unsigned)((a.Nq + kQPerBlock - 1) / kQPerBlock);
+  // scheduled calls (at most kSchedMaxClasses x 4096 items) take a 1-D grid
+  const dim3 grid = a.sched ? dim3(X * (unsigned)a.H * (unsigned)a.S) : dim3(X, (unsigned)a.H, (unsigned)a.S);
   stream_attention<<<grid, dim3(kAttnWaves * 64), 0, stream>>>(a);
   if (a.S > 1) {
     const size_t threads = (size_t)a.H * a.Nq * (kD / 8);

@@ -125,10 +125,58 @@ def test_long_cache_without_tile_skipping():
     # workspace: 64 KiB, the rotated keys (H * Nk * 128 bf16), the partials
     rot = (H * Nk * 128 * 2 + 255) // 256 * 256
     bounds = ((Nk + 31) // 32 * 8 + 255) // 256 * 256
+    assert (Nk + 31) // 32 > 1024  # past the dispatch schedule's limit: no schedule bytes
     S = (w.w4a8_stream_attention_workspace_bytes(H, Nq, Nk) - 64 * 1024 - rot - bounds) // (H * Nq * 130 * 4)
     assert S >= 1 and (Nk // 32) / S > 512
     rows = np.sort(np.random.Generator(np.random.PCG64(809)).choice(Nq, 64, replace=False))
     check(H, Hkv, pos_q, pos_k, 810, "long cache 1x10x4096", rows=rows)
+
+
+def test_dispatch_schedule():
+    # The key pre-pass deals the work items (query block, split, head) to
+    # workgroup ids: ranked by visible key tiles, heaviest first, dealt in
+    # rounds of one id per CU, every second full round reversed.  Read the
+    # schedule back from a caller workspace and compare it with that rule
+    # computed here from the positions; it must be a permutation, and the
+    # per-CU tile sums of the 4x4x192 window must stay within 10 % of the
+    # mean (94 against 87; the plain order gives up to 140).
+    V, F, T, H, Hkv = 4, 4, 192, 32, 8
+    pos_k, pos_q = window(V, F, T, 1)
+    Nq, Nk = len(pos_q), len(pos_k)
+    need = w.w4a8_stream_attention_workspace_bytes(H, Nq, Nk)
+    ws = torch.zeros(need, dtype=torch.uint8, device=dev())
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev()).view(torch.bfloat16)
+    q = I.activations(H * Nq, D, 811).reshape(H, Nq, D)
+    k = I.activations(Hkv * Nk, D, 812).reshape(Hkv, Nk, D)
+    cos_t, sin_t = oracle.rope_tables(Nk, D, base=1e6)
+    w.w4a8_stream_attention(t(q), t(k), t(k), torch.from_numpy(pos_q).to(dev()), torch.from_numpy(pos_k).to(dev()),
+                            torch.from_numpy(cos_t).to(dev()), torch.from_numpy(sin_t).to(dev()), 0.1, workspace=ws)
+    torch.cuda.synchronize()
+    X, ntiles = (Nq + 63) // 64, (Nk + 31) // 32
+    S = 2  # the split rule's choice here: 384 blocks x 2 fill one resident round
+    tps = (ntiles + S - 1) // S
+    G = X * S * H
+    off = 64 * 1024 + (H * Nk * 128 * 2 + 255) // 256 * 256 + (ntiles * 8 + 255) // 256 * 256
+    sched = ws[off:off + 4 * G].cpu().numpy().view(np.int32)
+    assert sorted(sched.tolist()) == list(range(G))
+    qmax = [pos_q[x * 64:(x + 1) * 64].max() for x in range(X)]
+    tmin = [pos_k[u * 32:(u + 1) * 32].min() for u in range(ntiles)]
+    vis = [sum(tmin[u] <= qmax[c // S] for u in range((c % S) * tps, min(ntiles, (c % S + 1) * tps)))
+           for c in range(X * S)]
+    order = sorted(range(X * S), key=lambda c: (-vis[c], c))
+    C = torch.cuda.get_device_properties(0).multi_processor_count
+    want = np.empty(G, np.int32)
+    for kk in range(G):
+        r, h = divmod(kk, H)
+        rnd, pp = divmod(kk, C)
+        rev = rnd % 2 == 1 and (rnd + 1) * C <= G
+        want[rnd * C + (C - 1 - pp if rev else pp)] = order[r] * H + h
+    assert np.array_equal(sched, want)
+    if C == 256:
+        cu = np.zeros(C)
+        for i, code in enumerate(sched):
+            cu[i % C] += vis[code // H]
+        assert cu.max() <= 1.10 * cu.mean(), (cu.min(), cu.mean(), cu.max())
 
 
 def test_rejected_calls():

@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <mutex>
 
+#include "attention.h"
 #include "kernels.h"
 
 using namespace w4a8;

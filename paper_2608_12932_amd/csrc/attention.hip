@@ -37,6 +37,7 @@
 #include <climits>
 
 #include "device.h"
+#include "attention.h"
 #include "kernels.h"
 
 namespace w4a8 {

@@ -93,32 +93,6 @@ typedef void (*LargeMKernelFn)(const LargeMArgs);
 // for any tile but the gated one)
 LargeMKernelFn largem_group_kernel(int cfg, bool swiglu);
 
-// ---- streaming prefill attention (attention.hip)
-struct AttnArgs {
-  const uint16_t* q;      // bf16 [H][Nq][128], before the rotary embedding
-  const uint16_t* k;      // bf16 [Hkv][Nk][128], before the rotary embedding
-  const uint16_t* v;      // bf16 [Hkv][Nk][128]
-  const int32_t* pos_q;   // [Nq] window positions
-  const int32_t* pos_k;   // [Nk]
-  const float* rope_cos;  // [n_pos][64]
-  const float* rope_sin;  // [n_pos][64]
-  uint16_t* o;            // bf16 [H][Nq][128]
-  int H, Hkv, Nq, Nk, n_pos;
-  float scale_log2e;      // score scale times log2(e)
-  void* workspace;        // rotated keys and split partials (stream_attention_workspace bytes)
-  // set by the launcher
-  uint16_t* k_rot;        // bf16 [Hkv][Nk][128]: the keys rotated at their positions
-  int2* tile_bounds;      // [ceil(Nk / 32)] smallest and largest key position of each 32-key tile
-  int* sched;             // [items] work item of each workgroup id, or nullptr (plain order)
-  int sched_cus;          // compute units the schedule deals to
-  int S, tiles_per_split;
-  float* part_o;          // [S][H][Nq][128] unnormalized partial sums
-  float* part_ml;         // [S][H][Nq][2] running maximum (base 2) and weight total
-};
-hipError_t launch_stream_attention(const AttnArgs& a, hipStream_t stream);
-int stream_attention_splits(int H, int Nq, int Nk);
-size_t stream_attention_workspace(int H, int Nq, int Nk);
-
 // ---- flow-matching Euler step with the velocity cache (flow.hip)
 // v == nullptr: a reused step (x += dt * cache); otherwise cache = v after
 // x += dt * v, and, with stats, stats[b] = (sum v c, sum v v, sum c c,

@@ -25,6 +25,7 @@ struct AttnArgs {
   int2* tile_bounds;      // [ceil(Nk / 32)] smallest and largest key position of each 32-key tile
   int* sched;             // [items] work item of each workgroup id, or nullptr (plain order)
   int sched_cus;          // compute units the schedule deals to
+  int* solo;              // [query blocks] the one split that sees keys of a block, else -1 (with sched)
   int S, tiles_per_split;
   float* part_o;          // [S][H][Nq][128] unnormalized partial sums
   float* part_ml;         // [S][H][Nq][2] running maximum (base 2) and weight total

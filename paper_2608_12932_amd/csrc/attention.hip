@@ -159,6 +159,17 @@ __device__ void build_schedule(const AttnArgs& a) {
     if (t < ntiles && s_tmin[t] <= s_qmax[c / S]) atomicAdd(&s_vis[c], 1);
   }
   __syncthreads();
+  // a block whose keys only one split sees: that split writes the output
+  // itself and the merge skips the block's rows
+  for (int x = tid; x < X; x += 256) {
+    int only = -1, cnt = 0;
+    for (int z = 0; z < S; ++z)
+      if (s_vis[x * S + z] > 0) {
+        ++cnt;
+        only = z;
+      }
+    a.solo[x] = cnt == 1 ? only : -1;
+  }
   // rank of each class: heavier first, ties in class order
   for (int c = tid; c < n; c += 256) {
     const int vc = s_vis[c];
@@ -259,6 +270,8 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
     xb = c / a.S;
     split = c % a.S;
   }
+  // this split alone sees keys of the block: it writes the output itself
+  const bool final_out = a.S == 1 || (a.sched && a.solo[xb] == split);
   const int hk = h / (a.H / a.Hkv);
   const int r16 = lane & 15, g = lane >> 4;
   const int P = a.n_pos;
@@ -475,7 +488,7 @@ __global__ __launch_bounds__(kAttnWaves * 64, 4) void stream_attention(const Att
   lsum += __shfl_xor(lsum, 16, 64);
   lsum += __shfl_xor(lsum, 32, 64);
   if (!q_ok) return;
-  if (a.S > 1) {
+  if (!final_out) {
     // a split's partial result: the unnormalized sum, its running maximum
     // (base 2, scaled scores) and weight total; attn_combine merges them
     const size_t row = ((size_t)split * a.H + h) * a.Nq + qi;
@@ -504,6 +517,7 @@ __global__ __launch_bounds__(256) void attn_combine(const AttnArgs a) {
   if (idx >= rows * (kD / 8)) return;
   const size_t row = idx / (kD / 8);
   const int c = (int)(idx % (kD / 8));
+  if (a.sched && a.solo[(int)(row % (size_t)a.Nq) / kQPerBlock] >= 0) return;  // written by its only split
   float mmax = -INFINITY;
   for (int s = 0; s < a.S; ++s) mmax = fmaxf(mmax, a.part_ml[((size_t)s * rows + row) * 2]);
   float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, l = 0.0f;
@@ -559,7 +573,8 @@ int used_splits(int H, int Nq, int Nk, int* tiles_per_split) {
 size_t schedule_bytes(int H, int Nq, int Nk) {
   const long classes = (long)((Nq + kQPerBlock - 1) / kQPerBlock) * used_splits(H, Nq, Nk, nullptr);
   if (classes > kSchedMaxClasses || (Nk + kKeys - 1) / kKeys > kSchedMaxTiles) return 0;
-  return ((size_t)classes * H * sizeof(int) + 255) / 256 * 256;
+  const size_t blocks = (size_t)(Nq + kQPerBlock - 1) / kQPerBlock;
+  return (((size_t)classes * H + blocks) * sizeof(int) + 255) / 256 * 256;  // the schedule, then the solo table
 }
 size_t stream_attention_workspace(int H, int Nq, int Nk) {
   const int S = stream_attention_splits(H, Nq, Nk);
@@ -591,6 +606,7 @@ hipError_t launch_stream_attention(const AttnArgs& a0, hipStream_t stream) {
   const size_t sched_bytes = schedule_bytes(a.H, a.Nq, a.Nk);
   a.sched = sched_bytes ? reinterpret_cast<int*>(ws + rotated_keys_bytes(a.H, a.Nk) + tile_bounds_bytes(a.Nk)) : nullptr;
   a.sched_cus = compute_units();
+  a.solo = a.sched ? a.sched + (size_t)((a.Nq + kQPerBlock - 1) / kQPerBlock) * a.S * a.H : nullptr;
   if (a.S > 1) {
     a.part_o = reinterpret_cast<float*>(ws + rotated_keys_bytes(a.H, a.Nk) + tile_bounds_bytes(a.Nk) + sched_bytes);
     a.part_ml = a.part_o + (size_t)a.S * a.H * a.Nq * kD;

@@ -191,10 +191,11 @@ def test_stream_attention_rejections():
     assert f(*args(Nq=0)) == w.W4A8_OK
     # the workspace: counter region, the rotated keys (room for H kv heads),
     # the tiles' position bounds (8 bytes per 32 keys), the dispatch schedule
-    # (4 bytes per work item: 12 query blocks x 2 splits x 32 heads), each in
-    # 256-byte units, then, for a shape that splits its key range, the partials
+    # (4 bytes per work item: 12 query blocks x 2 splits x 32 heads) and the
+    # per-block solo-split table (4 bytes per block), each region in 256-byte
+    # units, then, for a shape that splits its key range, the partials
     need = w.w4a8_stream_attention_workspace_bytes(32, 768, 3072)
-    assert need == 64 * 1024 + 32 * 3072 * 128 * 2 + 768 + 3072 + 2 * 32 * 768 * (128 + 2) * 4
+    assert need == 64 * 1024 + 32 * 3072 * 128 * 2 + 768 + 3328 + 2 * 32 * 768 * (128 + 2) * 4
     assert f(*args(H=32, Hkv=8, Nq=768, Nk=3072)) == w.W4A8_EINVAL
     assert f(*args(H=32, Hkv=8, Nq=768, Nk=3072, ws=P((1 << 20) + 16), wsb=need)) == w.W4A8_EINVAL  # misaligned
     assert w.w4a8_stream_attention_workspace_bytes(4, 64, 256) == 64 * 1024 + 4 * 256 * 128 * 2 + 256 + 256  # no split

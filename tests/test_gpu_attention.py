@@ -172,6 +172,11 @@ def test_dispatch_schedule():
         rev = rnd % 2 == 1 and (rnd + 1) * C <= G
         want[rnd * C + (C - 1 - pp if rev else pp)] = order[r] * H + h
     assert np.array_equal(sched, want)
+    # the solo table after it: the one split that sees keys of a block, else -1
+    solo = ws[off + 4 * G:off + 4 * G + 4 * X].cpu().numpy().view(np.int32)
+    nonempty = [[z for z in range(S) if vis[x * S + z] > 0] for x in range(X)]
+    assert solo.tolist() == [ne[0] if len(ne) == 1 else -1 for ne in nonempty]
+    assert (solo >= 0).any() and (solo < 0).any()  # both paths occur in this window
     if C == 256:
         cu = np.zeros(C)
         for i, code in enumerate(sched):

@@ -100,6 +100,18 @@ def test_cache_shorter_than_one_tile():
     check(2, 2, pos_q, pos_k, 805, "window 1x2x7")
 
 
+def test_lone_split_past_the_first():
+    # keys in descending position order, so the earliest positions sit in
+    # the last key split: the first query block (positions 0..63) sees keys
+    # of the last of 8 splits only and writes its output from that split;
+    # the second block (the largest positions) sees every split and goes
+    # through the merge
+    Nk = 4096
+    pos_k = (Nk - 1 - np.arange(Nk)).astype(np.int32)
+    pos_q = np.concatenate([np.arange(64), Nk - 64 + np.arange(64)]).astype(np.int32)
+    check(2, 1, pos_q, pos_k, 813, "lone split 7 of 8")
+
+
 def test_query_seeing_no_key_gets_zero():
     pos_k = np.arange(10, 110, dtype=np.int32)
     pos_q = np.array([5, 50, 3, 109], np.int32)

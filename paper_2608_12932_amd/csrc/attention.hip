@@ -98,14 +98,8 @@ __device__ __forceinline__ void rotate_chunks(uint4 a8, uint4 b8, const float* c
   hi = make_uint4(hw[0], hw[1], hw[2], hw[3]);
 }
 
-// The keys rotated at their window positions: k_rot[hk][j] from k[hk][j]
-// and pos_k[j], one 16-byte pair of chunks (d = 8 c .., 64 + 8 c ..) per
-// thread, 32 keys of one kv head per workgroup.  Rotating each key once
-// here instead of in every workgroup that stages it (all query blocks of
-// the kv head's query heads) took 21 us off the bench workload's 114 us.
 // Limits of the dispatch schedule (larger calls keep the plain order).
 constexpr int kSchedMaxClasses = 256;  // (query block, split) pairs
-constexpr int kRotHeads = 2;  // kv heads per thread of the key rotation
 constexpr int kSchedMaxTiles = 1024;   // 32-key tiles
 
 // The order in which the attention's workgroups take their work items.
@@ -192,6 +186,16 @@ __device__ void build_schedule(const AttnArgs& a) {
   }
 }
 
+constexpr int kRotHeads = 2;  // kv heads per thread of the key rotation
+
+// The keys rotated at their window positions: k_rot[hk][j] from k[hk][j]
+// and pos_k[j], one 16-byte pair of chunks (d = 8 c .., 64 + 8 c ..) of
+// kRotHeads kv heads per thread (one read of the table row), 32 keys per
+// workgroup.  Rotating each key once here instead of in every workgroup
+// that stages it (all query blocks of the kv head's query heads) took
+// 21 us off the bench workload's 114 us.  The first row of workgroups also
+// records each tile's key-position bounds, and one more workgroup, past
+// the last tile, builds the dispatch schedule.
 __global__ __launch_bounds__(256) void rotate_keys(const AttnArgs a) {
   const int tid = threadIdx.x, hk = blockIdx.y;
   if ((int)blockIdx.x * kKeys >= a.Nk) {  // the column past the last tile: the schedule

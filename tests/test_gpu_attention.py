@@ -112,6 +112,20 @@ def test_lone_split_past_the_first():
     check(2, 1, pos_q, pos_k, 813, "lone split 7 of 8")
 
 
+@pytest.mark.parametrize("H,Hkv,Nq", [(4, 2, 4096), (2, 1, 10240)])
+def test_schedule_limit(H, Hkv, Nq):
+    # 4096 keys in position order under Nq queries spread over them: 4 query
+    # heads x 4096 queries give 64 query blocks x 4 splits = 256 (block,
+    # split) pairs, the most the dispatch schedule deals (1024 workgroups);
+    # 2 heads x 10240 queries give 160 x 2 = 320 pairs, past it, so the plain
+    # grid with a merge runs (64 sampled queries each)
+    Nk = 4096
+    pos_k = np.arange(Nk, dtype=np.int32)
+    pos_q = np.sort(np.random.Generator(np.random.PCG64(814)).integers(0, Nk, Nq)).astype(np.int32)
+    rows = np.sort(np.random.Generator(np.random.PCG64(815)).choice(Nq, 64, replace=False))
+    check(H, Hkv, pos_q, pos_k, 816, f"schedule limit H={H} Nq={Nq}", rows=rows)
+
+
 def test_query_seeing_no_key_gets_zero():
     pos_k = np.arange(10, 110, dtype=np.int32)
     pos_q = np.array([5, 50, 3, 109], np.int32)

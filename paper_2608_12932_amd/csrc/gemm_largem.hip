@@ -38,6 +38,7 @@ LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu) {
   for (int c = 0; c < kMenuSize; ++c) {
     const TileCfg& t = kMenu[c];
     if (group && !t.group_ok) continue;
+    if (t.ks > 1) continue;  // the k-split form replaces entry 2 below
     if (swiglu ? !t.gated_ok : !t.plain_ok) continue;
     const int BM = 32 * t.WM * t.GM, BN = 32 * t.WN * t.GN;
     const int tm = (M + BM - 1) / BM, tn = swiglu ? (N / 2 + BN / 2 - 1) / (BN / 2) : (N + BN - 1) / BN;
@@ -50,14 +51,22 @@ LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu) {
       p.cfg = c;
       p.BM = BM;
       p.BN = BN;
-      p.threads = 64 * t.GM * t.GN;
+      p.threads = 64 * t.GM * t.GN * t.ks;
       p.tiles_m = tm;
       p.tiles_n = tn;
       p.tiles = tiles;
     }
   }
-  p.lds_bytes = (size_t)kMenu[p.cfg].ring * ((size_t)p.BM * 128 + (size_t)p.BN / 16 * kBlockBytes +
-                                             (group ? (size_t)p.threads / 64 * 256 : 0));
+  // group 64 x 64 tiles that fill at most one round: two k groups per tile
+  // (measured at M = 256: o 12.4 -> 10.8 us, down 31.8 -> 24.4 us; with more
+  // tiles, one 8-wave workgroup per CU loses to three 4-wave ones)
+  if (group && !swiglu && p.cfg == 2 && p.tiles <= 256) {
+    p.cfg = kMenuKSplit;
+    p.threads = 64 * kMenu[p.cfg].GM * kMenu[p.cfg].GN * kMenu[p.cfg].ks;
+  }
+  const TileCfg& c = kMenu[p.cfg];
+  p.lds_bytes = (size_t)c.ring * ((size_t)p.BM * 128 + (size_t)p.BN / 16 * kBlockBytes +
+                                  (group ? (size_t)(c.GM * c.GN) * 256 : 0));
   return p;
 }
 
@@ -71,8 +80,8 @@ hipError_t launch_largem(const LargeMPlan& p, const LargeMArgs& a, hipStream_t s
 
 const char* largem_kernel_name(const LargeMPlan& p) {
   static thread_local char buf[96];
-  snprintf(buf, sizeof buf, "largem<%dx%d,%s%s> tiles=%dx%d", p.BM, p.BN, p.group ? "group" : "channel",
-           p.swiglu ? ",swiglu" : "", p.tiles_m, p.tiles_n);
+  snprintf(buf, sizeof buf, "largem<%dx%d,%s%s%s> tiles=%dx%d", p.BM, p.BN, p.group ? "group" : "channel",
+           p.swiglu ? ",swiglu" : "", kMenu[p.cfg].ks > 1 ? ",ksplit" : "", p.tiles_m, p.tiles_n);
   return buf;
 }
 

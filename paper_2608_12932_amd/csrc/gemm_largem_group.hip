@@ -15,6 +15,7 @@ LargeMKernelFn largem_group_kernel(int cfg, bool swiglu) {
   switch (cfg) {
     case 1: return menu_kernel<1, true>();
     case 2: return menu_kernel<2, true>();
+    case kMenuKSplit: return menu_kernel<kMenuKSplit, true>();
     default: return nullptr;  // 128 x 192 does not fit the group accumulators
   }
 }

@@ -58,6 +58,7 @@ namespace {
 // them in flight to cover the L2 latency.
 struct TileCfg {
   int WM, WN, GM, GN, ring;
+  int ks;          // k groups of GM x GN waves (each with ring / ks stages)
   double quality;  // relative efficiency of the tile shape (operand reuse)
   bool group_ok;   // fits the registers with group-mode accumulators
   bool plain_ok;   // serves the plain output (its fp32 tile fits the LDS ring)
@@ -69,18 +70,29 @@ struct TileCfg {
 // 128 x 256 serves only the gated output: its plain fp32 tile (133 KB)
 // would not fit the 128 KB ring, the gated one (64 KB) does.
 constexpr TileCfg kMenu[] = {
-    {2, 3, 2, 2, 4, 1.00, false, true, false},  // 128 x 192, 4 waves
-    {2, 2, 2, 2, 4, 0.95, true, true, true},    // 128 x 128, 4 waves
-    {1, 1, 2, 2, 4, 0.80, true, true, false},   // 64 x 64, 4 waves
-    {2, 4, 2, 2, 4, 1.05, false, false, true},  // 128 x 256, 4 waves (gated)
+    {2, 3, 2, 2, 4, 1, 1.00, false, true, false},  // 128 x 192, 4 waves
+    {2, 2, 2, 2, 4, 1, 0.95, true, true, true},    // 128 x 128, 4 waves
+    {1, 1, 2, 2, 4, 1, 0.80, true, true, false},   // 64 x 64, 4 waves
+    {2, 4, 2, 2, 4, 1, 1.05, false, false, true},  // 128 x 256, 4 waves (gated)
+    // 64 x 64 in group mode with two k groups (8 waves, two per SIMD, an
+    // 8-deep ring): taken in place of entry 2 when the tiles fill at most
+    // one round, i.e. one workgroup per CU, where a single wave per SIMD
+    // leaves the SIMD idle between its rescale and MFMA bursts
+    {1, 1, 2, 2, 8, 2, 0.80, false, false, false},
 };
+constexpr int kMenuKSplit = 4;  // the k-split form of entry 2
 constexpr int kMenuSize = sizeof(kMenu) / sizeof(kMenu[0]);
 
-template <int WM, int WN, int GM, int GN, bool GROUP, int kRing, bool SW>
-__global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
+template <int WM, int WN, int GM, int GN, bool GROUP, int kRing, bool SW, int KS = 1>
+__global__ __launch_bounds__(GM * GN * 64 * KS) void largem(const LargeMArgs a) {
   static_assert(!SW || WN % 2 == 0, "gated tiles pair gate and up blocks per wave");
-  constexpr int kThreads = GM * GN * 64;
-  constexpr int kWaves = GM * GN;
+  // KS k groups of GM x GN waves: group wk takes the steps kb = KS i + wk
+  // with its own kRing / KS stages of the ring (stage KS s + wk), and the
+  // groups' sums meet in LDS at the end
+  constexpr int kThreads = GM * GN * 64;  // threads of one k group
+  constexpr int kWaves = GM * GN;         // waves of one k group
+  constexpr int kOwnRing = kRing / KS;    // ring stages of one k group
+  static_assert(kRing % KS == 0, "every k group owns whole ring stages");
   constexpr int BM = 32 * WM * GM, BN = 32 * WN * GN;
   constexpr int kABytes = BM * 128, kBBytes = BN / 16 * kBlockBytes;
   constexpr int kSBytes = GROUP ? kWaves * 256 : 0;  // group scales: 256 B per wave
@@ -90,7 +102,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   // address plus the stage's immediate offset (the activation region of a
   // 4-deep ring of 128-row tiles is exactly 64 KiB, the immediate's range).
   constexpr int kAReg = kRing * kABytes, kBReg = kRing * kBBytes;
-  static_assert(kRing == 4, "the step loop is unrolled over the 4 ring stages");
+  static_assert(kOwnRing == 4, "the step loop is unrolled over a k group's 4 ring stages");
   constexpr int kACh = kABytes / 16 / kThreads, kBCh = kBBytes / 16 / kThreads;  // loads per thread per stage
   static_assert(kACh * kThreads * 16 == kABytes, "A tile must split evenly over the threads");
   static_assert(kBCh * kThreads * 16 == kBBytes, "B tile must split evenly over the threads");
@@ -109,7 +121,8 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   constexpr int OBN = SW ? BN / 2 : BN;  // output columns per tile
   const int m0 = tm * BM, n0 = tn * BN, nt0 = n0 / 16;
   const int f0 = tn * OBN, ft0 = f0 / 16, fu0 = a.F / 16 + ft0;
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = (int)threadIdx.x % kThreads, lane = tid & 63;  // within the k group
+  const int wk = __builtin_amdgcn_readfirstlane((int)threadIdx.x / kThreads);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % GM, wn = wave / GM;
   const int M = a.M, N = a.N, K = a.K, KB = a.KB;
@@ -170,14 +183,14 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   auto issue_one = [&](int kb, int stage, int d) {
     const bool ok = kb < KB;
     if (d < kACh) {
-      lds_dma16(ares, lds_base + (uint32_t)(stage * kABytes + (d * kWaves + wave) * 1024), a_voff[d],
+      lds_dma16(ares, lds_base + (uint32_t)((KS * stage + wk) * kABytes + (d * kWaves + wave) * 1024), a_voff[d],
                 ok ? kb * 128 : kOOB);
     } else if (d < kACh + kBCh) {
       const int blk = (d - kACh) * kWaves + wave;
-      lds_dma16_nt(b_up[d - kACh] ? bres_u : bres, lds_base + (uint32_t)(kAReg + stage * kBBytes + blk * 1024),
+      lds_dma16_nt(b_up[d - kACh] ? bres_u : bres, lds_base + (uint32_t)(kAReg + (KS * stage + wk) * kBBytes + blk * 1024),
                    b_voff[d - kACh], ok ? kb * kBlockBytes : kOOB);
     } else if constexpr (GROUP) {
-      lds_dma4(s_up ? sres_u : sres, lds_base + (uint32_t)(kAReg + kBReg + stage * kSBytes + wave * 256), s_voff,
+      lds_dma4(s_up ? sres_u : sres, lds_base + (uint32_t)(kAReg + kBReg + (KS * stage + wk) * kSBytes + wave * 256), s_voff,
                ok ? (uint32_t)((size_t)kb * N * 2) : kOOB);
     }
   };
@@ -194,11 +207,11 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   const int swz = (l32 >> 1) & 7;
   uint32_t a_rd[WM], b_rd[WN];
 #pragma unroll
-  for (int i = 0; i < WM; ++i) a_rd[i] = (uint32_t)((wm * 32 * WM + i * 32 + l32) * 128);
+  for (int i = 0; i < WM; ++i) a_rd[i] = (uint32_t)(wk * kABytes + (wm * 32 * WM + i * 32 + l32) * 128);
 #pragma unroll
   for (int j = 0; j < WN; ++j) {
     const int col = tile_col(j);
-    b_rd[j] = (uint32_t)(kAReg + (col >> 4) * kBlockBytes + (col & 15) * 16);
+    b_rd[j] = (uint32_t)(kAReg + wk * kBBytes + (col >> 4) * kBlockBytes + (col & 15) * 16);
   }
   // MFMA k half tp covers the 64 k of chunk group g = 2 tp + g2: activation
   // chunks 2 g and 2 g + 1, weight chunk g (low nibbles, then high nibbles).
@@ -218,7 +231,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
   for (int j = 0; j < (GROUP ? WN : 1); ++j) {
     const int col = tile_col(j);
-    s_rd[j] = (uint32_t)(kAReg + kBReg + (col / kSPerWave) * 256 + (col % kSPerWave) * 2);
+    s_rd[j] = (uint32_t)(kAReg + kBReg + wk * kSBytes + (col / kSPerWave) * 256 + (col % kSPerWave) * 2);
   }
 
   // One step's MFMA operands, held in registers so that the LDS reads of
@@ -242,7 +255,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
     if (r < 2 * kReadsTp) {
       const int tp = r / kReadsTp, u = r % kReadsTp;
       if (u < WN)
-        o.b[u][tp] = *reinterpret_cast<const uint4*>(lds + S * kBBytes + b_rd[u] + (2 * tp + g2) * 256);
+        o.b[u][tp] = *reinterpret_cast<const uint4*>(lds + S * KS * kBBytes + b_rd[u] + (2 * tp + g2) * 256);
       else if constexpr (GROUP) {
         // Group mode reads the activation operands straight into AGPRs
         // (only the MFMA reads them), which leaves the VGPRs to the int32
@@ -250,15 +263,15 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
         // whose barrier waits for every outstanding LDS read.
         const uint32_t addr = lds_base + a_addr[(u - WN) / 2][2 * tp + ((u - WN) & 1)];
         v4i t;
-        asm volatile("ds_read_b128 %0, %1 offset:%2" : "=a"(t) : "v"(addr), "i"(S * kABytes) : "memory");
+        asm volatile("ds_read_b128 %0, %1 offset:%2" : "=a"(t) : "v"(addr), "i"(S * KS * kABytes) : "memory");
         o.a[(u - WN) / 2][2 * tp + ((u - WN) & 1)] = t;
       } else {
         o.a[(u - WN) / 2][2 * tp + ((u - WN) & 1)] =
-            *reinterpret_cast<const v4i*>(lds + S * kABytes + a_addr[(u - WN) / 2][2 * tp + ((u - WN) & 1)]);
+            *reinterpret_cast<const v4i*>(lds + S * KS * kABytes + a_addr[(u - WN) / 2][2 * tp + ((u - WN) & 1)]);
       }
     } else if constexpr (GROUP) {
       const int j = r - 2 * kReadsTp;
-      o.sg[j] = f16_to_f32(*reinterpret_cast<const uint16_t*>(lds + S * kSBytes + s_rd[j])) * 0.0625f;
+      o.sg[j] = f16_to_f32(*reinterpret_cast<const uint16_t*>(lds + S * KS * kSBytes + s_rd[j])) * 0.0625f;
     }
   };
 
@@ -354,7 +367,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   for (int j = 0; j < (GROUP ? WN : 1); ++j) sg_prev[j] = 0.0f;
   auto step = [&](auto stage_c, int kb, const Ops& cur, Ops& nxt, v16i (&c)[WM][WN], v16i (&prev)[WM][WN]) {
     constexpr int S = decltype(stage_c)::value;
-    wait_vmcnt<(kRing - 2) * kPerStage>();
+    wait_vmcnt<(kOwnRing - 2) * kPerStage>();
     lds_barrier();
     v4i lo1[WN], hi1[WN];
 #pragma unroll
@@ -373,7 +386,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
         if (d * kMfma / kPerStage == q) issue_one(kb + kRing, S, d);
 #pragma unroll
       for (int r = 0; r < kReads; ++r)
-        if (r * kMfma / kReads == q) read_one(std::integral_constant<int, (S + 1) % kRing>{}, r, nxt);
+        if (r * kMfma / kReads == q) read_one(std::integral_constant<int, (S + 1) % kOwnRing>{}, r, nxt);
 #pragma unroll
       for (int u = 0; u < kUnits; ++u) {
         if (q < kHalf && u * kHalf / kUnits == q) unpack_word(cur.b[u / 4][1], u % 4, lo1[u / 4], hi1[u / 4]);
@@ -420,7 +433,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   for (int j = 0; j < (GROUP ? WN : 1); ++j) sg_last[j] = 0.0f;
   auto step1 = [&](auto stage_c, int kb, const Ops& cur, Ops& nxt, v16i (&c)[WM][WN]) {
     constexpr int S = decltype(stage_c)::value;
-    wait_vmcnt<(kRing - 2) * kPerStage>();
+    wait_vmcnt<(kOwnRing - 2) * kPerStage>();
     lds_barrier();
 #pragma unroll
     for (int q = 0; q < kMfma; ++q) {
@@ -436,7 +449,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
         if (d * kMfma / kPerStage == q) issue_one(kb + kRing, S, d);
 #pragma unroll
       for (int r = 0; r < kReads; ++r)
-        if (r * kMfma / kReads == q) read_one(std::integral_constant<int, (S + 1) % kRing>{}, r, nxt);
+        if (r * kMfma / kReads == q) read_one(std::integral_constant<int, (S + 1) % kOwnRing>{}, r, nxt);
 #pragma unroll
       for (int u = 0; u < kUnits; ++u) {
         if (q == kMfma * 3 / 16 + u * (kMfma * 6 / 16) / kUnits)
@@ -451,12 +464,13 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
     for (int j = 0; j < (GROUP ? WN : 1); ++j) sg_last[j] = cur.sg[j];
   };
 
+  const int NS = (KB + KS - 1) / KS;  // steps per k group (a trailing one past K reads zeros)
 #pragma unroll
-  for (int st = 0; st < kRing; ++st)
+  for (int st = 0; st < kOwnRing; ++st)
 #pragma unroll
-    for (int d = 0; d < kPerStage; ++d) issue_one(st, st, d);
+    for (int d = 0; d < kPerStage; ++d) issue_one(KS * st + wk, st, d);
   Ops o0, o1;
-  wait_vmcnt<(kRing - 1) * kPerStage>();  // stage 0 (and the scales, issued before it)
+  wait_vmcnt<(kOwnRing - 1) * kPerStage>();  // stage 0 (and the scales, issued before it)
   lds_barrier();
 #pragma unroll
   for (int r = 0; r < kReads; ++r) read_one(std::integral_constant<int, 0>{}, r, o0);
@@ -465,21 +479,21 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   if constexpr (GROUP && kMfma >= 12) {
 #pragma unroll
     for (int u = 0; u < kUnits; ++u) unpack_word(o0.b[u / 4][1], u % 4, o0.lo1[u / 4], o0.hi1[u / 4]);
-    for (int kb = 0; kb < KB; kb += kRing) {
-      step1(std::integral_constant<int, 0>{}, kb, o0, o1, acc[0]);
-      if (kb + 1 < KB) step1(std::integral_constant<int, 1>{}, kb + 1, o1, o0, acc[0]);
-      if (kb + 2 < KB) step1(std::integral_constant<int, 2>{}, kb + 2, o0, o1, acc[0]);
-      if (kb + 3 < KB) step1(std::integral_constant<int, 3>{}, kb + 3, o1, o0, acc[0]);
+    for (int i = 0; i < NS; i += kOwnRing) {
+      step1(std::integral_constant<int, 0>{}, KS * i + wk, o0, o1, acc[0]);
+      if (i + 1 < NS) step1(std::integral_constant<int, 1>{}, KS * (i + 1) + wk, o1, o0, acc[0]);
+      if (i + 2 < NS) step1(std::integral_constant<int, 2>{}, KS * (i + 2) + wk, o0, o1, acc[0]);
+      if (i + 3 < NS) step1(std::integral_constant<int, 3>{}, KS * (i + 3) + wk, o1, o0, acc[0]);
     }
     // the last step's rescales that fall past its last slot
 #pragma unroll
     for (int q = 0; q < kMfma; ++q) rescale_slot(q, true, acc[0], sg_last);
   } else {
-    for (int kb = 0; kb < KB; kb += kRing) {
-      step(std::integral_constant<int, 0>{}, kb, o0, o1, acc[0], acc[GROUP ? 1 : 0]);
-      if (kb + 1 < KB) step(std::integral_constant<int, 1>{}, kb + 1, o1, o0, acc[GROUP ? 1 : 0], acc[0]);
-      if (kb + 2 < KB) step(std::integral_constant<int, 2>{}, kb + 2, o0, o1, acc[0], acc[GROUP ? 1 : 0]);
-      if (kb + 3 < KB) step(std::integral_constant<int, 3>{}, kb + 3, o1, o0, acc[GROUP ? 1 : 0], acc[0]);
+    for (int i = 0; i < NS; i += kOwnRing) {
+      step(std::integral_constant<int, 0>{}, KS * i + wk, o0, o1, acc[0], acc[GROUP ? 1 : 0]);
+      if (i + 1 < NS) step(std::integral_constant<int, 1>{}, KS * (i + 1) + wk, o1, o0, acc[GROUP ? 1 : 0], acc[0]);
+      if (i + 2 < NS) step(std::integral_constant<int, 2>{}, KS * (i + 2) + wk, o0, o1, acc[0], acc[GROUP ? 1 : 0]);
+      if (i + 3 < NS) step(std::integral_constant<int, 3>{}, KS * (i + 3) + wk, o1, o0, acc[GROUP ? 1 : 0], acc[0]);
     }
   }
   if constexpr (GROUP && kMfma < 12) {
@@ -492,7 +506,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) facc[i][j][r] = __fmaf_rn((float)last[i][j][r], sg_prev[j], facc[i][j][r]);
     };
-    if (KB & 1)
+    if (NS & 1)
       rescale_last(acc[0]);
     else
       rescale_last(acc[1]);
@@ -500,6 +514,30 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
   if constexpr (GROUP) load_sx();
   wait_vmcnt<0>();  // the stages issued past the end (and group mode's token scales)
   lds_barrier();    // every wave is done with the ring
+  if constexpr (KS > 1) {
+    // the k groups' fp32 sums meet in the idle ring; group 0 keeps the total
+    static_assert(GROUP, "k groups merge fp32 group-mode sums");
+    static_assert((KS - 1) * kWaves * WM * WN * 16 * 64 * 4 <= kRing * kStage, "merge must fit the ring");
+    float* red = reinterpret_cast<float*>(lds);
+    auto slot = [&](int g, int i, int j, int r) { return ((((g * kWaves + wave) * WM + i) * WN + j) * 16 + r) * 64 + lane; };
+    if (wk > 0)
+#pragma unroll
+      for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) red[slot(wk - 1, i, j, r)] = facc[i][j][r];
+    lds_barrier();
+    if (wk == 0)
+      for (int g = 1; g < KS; ++g)
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+#pragma unroll
+          for (int j = 0; j < WN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) facc[i][j][r] = __fadd_rn(facc[i][j][r], red[slot(g - 1, i, j, r)]);
+    lds_barrier();
+  }
 
   // ---- epilogue.  Lane holds column l32 and rows 8 q + 4 g2 + e (r = 4 q + e)
   // of each 32 x 32 block.  The scaled tile is staged in the idle LDS ring
@@ -544,6 +582,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
       // own 2-3}.
       const bool odd = lane & 1;
       const uint32_t sel = odd ? 0x03020706u : 0x05040100u;
+      if (wk == 0)
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
@@ -560,6 +599,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
             *reinterpret_cast<uint32_t*>(lds + row * kPitch + col * 2) = word;
           }
     } else {
+      if (wk == 0)
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
@@ -579,10 +619,10 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
     lds_barrier();
     constexpr int kRowChunks = OBN * es / 16;
     constexpr int kChunks = BM * kRowChunks;
-    static_assert(kChunks % kThreads == 0, "output chunks must split evenly over the threads");
+    static_assert(kChunks % (kThreads * KS) == 0, "output chunks must split evenly over the threads");
 #pragma unroll
-    for (int it = 0; it < kChunks / kThreads; ++it) {
-      const int p = it * kThreads + tid;
+    for (int it = 0; it < kChunks / (kThreads * KS); ++it) {
+      const int p = it * kThreads * KS + (int)threadIdx.x;
       const int row = p / kRowChunks, cc = p % kRowChunks;
       const uint4 v = *reinterpret_cast<const uint4*>(lds + row * kPitch + cc * 16);
       // N is a multiple of 16 and a chunk holds 4 or 8 columns, so a chunk
@@ -600,7 +640,7 @@ __global__ __launch_bounds__(GM * GN * 64) void largem(const LargeMArgs a) {
 // The instance of menu entry C (SW: the gated form).
 template <int C, bool GROUP, bool SW = false>
 constexpr LargeMKernelFn menu_kernel() {
-  return largem<kMenu[C].WM, kMenu[C].WN, kMenu[C].GM, kMenu[C].GN, GROUP, kMenu[C].ring, SW>;
+  return largem<kMenu[C].WM, kMenu[C].WN, kMenu[C].GM, kMenu[C].GN, GROUP, kMenu[C].ring, SW, kMenu[C].ks>;
 }
 
 }  // namespace

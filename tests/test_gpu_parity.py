@@ -168,6 +168,18 @@ def test_large_m_every_ring_remainder(M, K, N, group):
     check_all_outputs(x, W, s, group=group, label="large-M ring remainder")
 
 
+@pytest.mark.parametrize("M,K,N", [(70, 65536, 96), (130, 12288, 4096)])
+def test_large_m_k_split_long_k(M, K, N):
+    # group tiles that fill at most one round run with two k groups of waves
+    # merged at the end: the longest K (256 steps per group) and a down
+    # projection at a ragged M (sampled rows)
+    assert "ksplit" in w.w4a8_linear_describe(M, N, K, 1)
+    x = I.activations(M, K, 820 + M)
+    W, s = I.weights(N, K, 821 + N, group=True)
+    rows = None if N < 1024 else np.arange(0, M, 7)
+    check_all_outputs(x, W, s, group=True, rows=rows, label="large-M k split")
+
+
 # ------------------------------------------------------------ split-K, determinism, workspace reuse
 
 @pytest.mark.parametrize("M,N", [(16, 32), (1, 16)])

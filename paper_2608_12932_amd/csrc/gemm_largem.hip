@@ -21,6 +21,7 @@ LargeMKernelFn channel_kernel(int cfg, bool swiglu) {
     case 0: return menu_kernel<0, false>();
     case 1: return menu_kernel<1, false>();
     case 2: return menu_kernel<2, false>();
+    case kMenuKSplit: return menu_kernel<kMenuKSplit, false>();
     default: return nullptr;
   }
 }
@@ -57,10 +58,11 @@ LargeMPlan plan_largem(int M, int N, int K, bool group, bool swiglu) {
       p.tiles = tiles;
     }
   }
-  // group 64 x 64 tiles that fill at most one round: two k groups per tile
-  // (measured at M = 256: o 12.4 -> 10.8 us, down 31.8 -> 24.4 us; with more
-  // tiles, one 8-wave workgroup per CU loses to three 4-wave ones)
-  if (group && !swiglu && p.cfg == 2 && p.tiles <= 256) {
+  // 64 x 64 tiles that fill at most one round: two k groups per tile
+  // (measured at M = 256, group scales: o 12.4 -> 10.8 us, down 31.8 -> 24.4
+  // us; channel scales: down 24.0 -> 21.7 us, o unchanged; with more tiles,
+  // one 8-wave workgroup per CU loses to three 4-wave ones)
+  if (!swiglu && p.cfg == 2 && p.tiles <= 256) {
     p.cfg = kMenuKSplit;
     p.threads = 64 * kMenu[p.cfg].GM * kMenu[p.cfg].GN * kMenu[p.cfg].ks;
   }

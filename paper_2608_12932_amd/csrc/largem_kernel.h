@@ -74,10 +74,10 @@ constexpr TileCfg kMenu[] = {
     {2, 2, 2, 2, 4, 1, 0.95, true, true, true},    // 128 x 128, 4 waves
     {1, 1, 2, 2, 4, 1, 0.80, true, true, false},   // 64 x 64, 4 waves
     {2, 4, 2, 2, 4, 1, 1.05, false, false, true},  // 128 x 256, 4 waves (gated)
-    // 64 x 64 in group mode with two k groups (8 waves, two per SIMD, an
-    // 8-deep ring): taken in place of entry 2 when the tiles fill at most
-    // one round, i.e. one workgroup per CU, where a single wave per SIMD
-    // leaves the SIMD idle between its rescale and MFMA bursts
+    // 64 x 64 with two k groups (8 waves, two per SIMD, an 8-deep ring):
+    // taken in place of entry 2 when the tiles fill at most one round, i.e.
+    // one workgroup per CU, where a single wave per SIMD leaves the SIMD
+    // idle between its MFMA and VALU bursts
     {1, 1, 2, 2, 8, 2, 0.80, false, false, false},
 };
 constexpr int kMenuKSplit = 4;  // the k-split form of entry 2
@@ -515,10 +515,12 @@ __global__ __launch_bounds__(GM * GN * 64 * KS) void largem(const LargeMArgs a) 
   wait_vmcnt<0>();  // the stages issued past the end (and group mode's token scales)
   lds_barrier();    // every wave is done with the ring
   if constexpr (KS > 1) {
-    // the k groups' fp32 sums meet in the idle ring; group 0 keeps the total
-    static_assert(GROUP, "k groups merge fp32 group-mode sums");
+    // the k groups' sums (fp32 in group mode, int32 otherwise) meet in the
+    // idle ring; group 0 keeps the total
     static_assert((KS - 1) * kWaves * WM * WN * 16 * 64 * 4 <= kRing * kStage, "merge must fit the ring");
+    static_assert(!SW, "gated tiles take one k group");
     float* red = reinterpret_cast<float*>(lds);
+    int* redi = reinterpret_cast<int*>(lds);
     auto slot = [&](int g, int i, int j, int r) { return ((((g * kWaves + wave) * WM + i) * WN + j) * 16 + r) * 64 + lane; };
     if (wk > 0)
 #pragma unroll
@@ -526,7 +528,12 @@ __global__ __launch_bounds__(GM * GN * 64 * KS) void largem(const LargeMArgs a) 
 #pragma unroll
         for (int j = 0; j < WN; ++j)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) red[slot(wk - 1, i, j, r)] = facc[i][j][r];
+          for (int r = 0; r < 16; ++r) {
+            if constexpr (GROUP)
+              red[slot(wk - 1, i, j, r)] = facc[i][j][r];
+            else
+              redi[slot(wk - 1, i, j, r)] = acc[0][i][j][r];
+          }
     lds_barrier();
     if (wk == 0)
       for (int g = 1; g < KS; ++g)
@@ -535,7 +542,12 @@ __global__ __launch_bounds__(GM * GN * 64 * KS) void largem(const LargeMArgs a) 
 #pragma unroll
           for (int j = 0; j < WN; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) facc[i][j][r] = __fadd_rn(facc[i][j][r], red[slot(g - 1, i, j, r)]);
+            for (int r = 0; r < 16; ++r) {
+              if constexpr (GROUP)
+                facc[i][j][r] = __fadd_rn(facc[i][j][r], red[slot(g - 1, i, j, r)]);
+              else
+                acc[0][i][j][r] += redi[slot(g - 1, i, j, r)];
+            }
     lds_barrier();
   }
 

@@ -683,6 +683,221 @@ def profile_workload(spec: str, steps: int, warmup: int):
             "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1), "kernels": kinds}
 
 
+# ---- rocprofv3 summaries (profiles/<name>.txt) -------------------------------
+# Each summary comes from separate rocprofv3 runs of `bench.py --profile SPEC`
+# (a kernel trace, then FETCH_SIZE, then WRITE_SIZE, and at large M one pass
+# of MFMA / VALU counters; counters are never combined with tracing), and
+# `bench.py --summarize-profile NAME --prof-dir DIR` turns their CSV files
+# into the summary.  `--profile-commands NAME --prof-dir DIR` prints the
+# rocprofv3 commands, one per line.
+
+PROFILE_SPECS = {
+    "smallm_gate_up_verify": ("gate_up", "gate+up verify, M=16 K=4096 N=24576, per-channel scales; GEMM on int8 codes"),
+    "largem_qkv_prefill": ("qkv", "qkv prefill, M=1024 K=4096 N=6144, per-channel scales; GEMM on int8 codes"),
+    "smallm_down_verify_m1": ("down:1", "down verify, M=1 K=12288 N=4096, per-channel scales; GEMM on int8 codes"),
+    "smallm_down_verify_m4": ("down:4", "down verify, M=4 K=12288 N=4096, per-channel scales; GEMM on int8 codes"),
+    "smallm_down_verify_m16": ("down:16", "down verify, M=16 K=12288 N=4096, per-channel scales; GEMM on int8 codes"),
+    "smallm_group_layer_m1": ("layer:1", "decoder layer with group-128 fp16 scales, M=1: small-M GEMMs"),
+    "smallm_group_layer_m16": ("layer:16", "decoder layer with group-128 fp16 scales, M=16: small-M GEMMs"),
+    "largem_group_layer_m256": ("layer:256", "decoder layer with group-128 fp16 scales, M=256: large-M GEMMs"),
+    "largem_group_layer_m2048": ("layer:2048", "decoder layer with group-128 fp16 scales, M=2048: large-M GEMMs"),
+}
+MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_I8 SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU SQ_BUSY_CYCLES "
+                 "SQ_ACTIVE_INST_VALU SQ_WAIT_INST_LDS SQ_INSTS_MFMA GRBM_GUI_ACTIVE")
+N_SIMDS, N_XCDS = 1024, 8  # MI355X: 256 CUs x 4 SIMDs, 8 XCDs
+
+
+def _profile_gemms(spec: str):
+    """The GEMMs one profiled step launches, in order: (label, M, N, K, group),
+    and the packed-weight bytes of the matrix whose device clones calibrate
+    the counters (the largest one the run clones)."""
+    from paper_2608_12932_amd import inputs as I
+
+    kind, _, arg = spec.partition(":")
+    if kind == "gate_up":
+        g = [("", 16, 24576, 4096, False)]
+    elif kind == "qkv":
+        g = [("", 1024, 6144, 4096, False)]
+    elif kind == "down":
+        g = [("", int(arg), 4096, 12288, False)]
+    elif kind == "layer":
+        g = [(name, int(arg), N, K, True) for name, K, N in I.LAYER_MATS]
+    else:
+        raise SystemExit(f"unknown profile workload {spec!r}")
+    return g, max(N * K // 2 for _, _, N, K, _ in g)
+
+
+def profile_commands(name: str, out_dir: str):
+    spec = PROFILE_SPECS[name][0]
+    large = any(M > 64 for _, M, _, _, _ in _profile_gemms(spec)[0])
+    run = f"-o p --output-format csv -- python3 bench.py --profile {spec}"
+    cmds = [f"rocprofv3 --kernel-trace --stats -d {out_dir}/{name}_trace {run} --steps 100 --warmup 10",
+            f"rocprofv3 --pmc FETCH_SIZE -d {out_dir}/{name}_fetch {run} --steps 20 --warmup 3",
+            f"rocprofv3 --pmc WRITE_SIZE -d {out_dir}/{name}_write {run} --steps 20 --warmup 3"]
+    if large:
+        cmds.append(f"rocprofv3 --pmc {MFMA_COUNTERS} -d {out_dir}/{name}_mfma {run} --steps 20 --warmup 3")
+    return cmds
+
+
+def _csv_rows(run_dir: str, suffix: str):
+    import csv
+    import glob
+
+    files = sorted(glob.glob(os.path.join(run_dir, "**", f"*{suffix}"), recursive=True))
+    if not files:
+        raise SystemExit(f"no {suffix} under {run_dir}")
+    with open(files[0], newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _short_kernel(full: str) -> str:
+    """'void w4a8::(anonymous namespace)::smallm<1, 6, ...>(args)' -> 'smallm<1, 6, ...>'."""
+    name = full.split("(anonymous namespace)::")[-1]
+    depth, out = 0, []
+    for ch in name:
+        if ch == "(" and depth == 0:
+            break
+        depth += ch == "<"
+        depth -= ch == ">"
+        out.append(ch)
+    return "".join(out)
+
+
+def _is_gemm(kernel: str) -> bool:
+    k = _short_kernel(kernel)
+    return k.startswith("smallm<") or k.startswith("largem<")
+
+
+def _per_dispatch(rows, counter: str):
+    """{dispatch id: (kernel name, value)} for one counter of a --pmc run."""
+    out = {}
+    for r in rows:
+        if r["Counter_Name"] == counter:
+            out[int(r["Dispatch_Id"])] = (r["Kernel_Name"], float(r["Counter_Value"]))
+    return [out[d] for d in sorted(out)]
+
+
+def _calibration(rows, counter: str, nbytes: int):
+    """The factor that turns `counter` (KiB per dispatch) into bytes, from the
+    run's own device copies (__amd_rocclr_copyBuffer) of its largest weight,
+    nbytes: the copies whose count is within 10 % of the largest one (the
+    weights of one run differ by 1.5x or more)."""
+    import statistics
+
+    copies = [v for k, v in _per_dispatch(rows, counter) if "copyBuffer" in k]
+    if not copies:
+        raise SystemExit(f"no device copies to calibrate {counter}")
+    vals = [v for v in copies if v >= 0.9 * max(copies)]
+    return nbytes / (statistics.median(vals) * 1024), len(vals)
+
+
+def summarize_profile(name: str, out_dir: str) -> str:
+    import statistics
+
+    spec, desc = PROFILE_SPECS[name]
+    gemms, cal_bytes = _profile_gemms(spec)
+    ng = len(gemms)
+    cmds = profile_commands(name, out_dir)
+    trace = sorted(_csv_rows(os.path.join(out_dir, f"{name}_trace"), "kernel_trace.csv"),
+                   key=lambda r: int(r["Start_Timestamp"]))
+    durs = [(r["Kernel_Name"], (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3) for r in trace]
+    gemm_durs = [(k, d) for k, d in durs if _is_gemm(k)]
+    quant = [(k, d) for k, d in durs if "quantize_rows" in k]
+    fetch_rows = _csv_rows(os.path.join(out_dir, f"{name}_fetch"), "counter_collection.csv")
+    write_rows = _csv_rows(os.path.join(out_dir, f"{name}_write"), "counter_collection.csv")
+    ff, nf = _calibration(fetch_rows, "FETCH_SIZE", cal_bytes)
+    wf, nw = _calibration(write_rows, "WRITE_SIZE", cal_bytes)
+    fetch = [v for k, v in _per_dispatch(fetch_rows, "FETCH_SIZE") if _is_gemm(k)]
+    write = [v for k, v in _per_dispatch(write_rows, "WRITE_SIZE") if _is_gemm(k)]
+    mfma = None
+    if len(cmds) == 4:
+        mrows = _csv_rows(os.path.join(out_dir, f"{name}_mfma"), "counter_collection.csv")
+        mfma = {c: [v for k, v in _per_dispatch(mrows, c) if _is_gemm(k)] for c in MFMA_COUNTERS.split()}
+
+    lines = [f"# rocprofv3 summary: {desc}",
+             "# commands (each a separate run; counters never combined with tracing), from the repository root after",
+             "#   cd /tmp && export TMPDIR=/tmp:"]
+    lines += [f"#   {c}" for c in cmds]
+    if ng == 1 and spec.split(":")[0] in ("gate_up", "qkv"):
+        lines.append("# the profiled run times the bf16-in step (quantize launch + GEMM) and then the GEMM alone on "
+                     f"int8 codes;\n#   the GEMM kernel's durations below cover both ({len(gemm_durs)} dispatches "
+                     "incl. warmup)")
+    elif ng == 1:
+        lines.append("# the profiled run times the bf16-in step (quantize launch + GEMM on its codes); "
+                     f"{len(gemm_durs)} GEMM dispatches incl. warmup")
+    else:
+        qa = statistics.mean(d for _, d in quant) if quant else 0.0
+        lines.append("# a step is the four linears in order, each a quantize launch + GEMM on bf16 x; GEMM "
+                     "dispatches are\n#   assigned to the matrices by their order; "
+                     f"{len(quant)} quantize dispatches average {qa:.3f} us")
+    lines.append("# HBM bytes: FETCH_SIZE and WRITE_SIZE (KiB per dispatch) calibrated on __amd_rocclr_copyBuffer "
+                 f"copying a\n#   {cal_bytes} B packed weight in the same runs: FETCH factor {ff:.4f} ({nf} copies), "
+                 f"WRITE factor {wf:.4f} ({nw} copies)")
+
+    def stats_for(i):
+        sel = lambda seq: [x for j, x in enumerate(seq) if j % ng == i]
+        d = sel(gemm_durs)
+        us = [x for _, x in d]
+        label, M, N, K, group = gemms[i]
+        scale_bytes = (K // 128) * N * 2 if group else N * 4
+        algo = N * K // 2 + scale_bytes + M * K + 4 * M + 2 * M * N
+        ops = 2 * M * N * K
+        avg = statistics.mean(us)
+        fb = statistics.median(sel(fetch)) * 1024 * ff
+        wb = statistics.median(sel(write)) * 1024 * wf
+        out = [("kernel", _short_kernel(d[0][0])), ("avg_us", f"{avg:.3f}")]
+        if ng == 1:
+            out += [("median_us", f"{statistics.median(us):.3f}"), ("min_us", f"{min(us):.3f}")]
+        out.append(("calls", str(len(us))))
+        if ng == 1 and quant:
+            out += [("quantize_kernel", _short_kernel(quant[0][0])),
+                    ("quantize_avg_us", f"{statistics.mean(x for _, x in quant):.3f}")]
+        out.append(("algorithmic_bytes_per_dispatch", str(algo)))
+        if ng == 1:
+            out.append(("achieved_GBps_from_avg", f"{algo / avg / 1e3:.1f}"))
+        out.append(("frac_of_8TBps_from_avg", f"{algo / avg / 1e3 / HBM_PEAK_GBS:.4f}"))
+        if ng == 1:
+            out += [("int8_ops_per_dispatch", str(ops)), ("achieved_TOPS_from_avg", f"{ops / avg / 1e6:.1f}")]
+        out.append(("frac_of_5POPS_from_avg", f"{ops / avg / 1e6 / INT8_PEAK_TOPS:.4f}"))
+        if ng == 1:
+            out += [("fetch_bytes_per_dispatch", f"{fb:.0f}"), ("write_bytes_per_dispatch", f"{wb:.0f}")]
+        out += [("hbm_bytes_per_dispatch", f"{fb + wb:.0f}"), ("traffic_over_algorithmic", f"{(fb + wb) / algo:.3f}")]
+        if mfma:
+            med = {c: statistics.median(sel(v)) for c, v in mfma.items()}
+            gui = med["GRBM_GUI_ACTIVE"] / N_XCDS
+            out += [("mfma_int8_ops_per_dispatch",
+                     f"{med['SQ_INSTS_VALU_MFMA_MOPS_I8'] * 512:.0f}   (SQ_INSTS_VALU_MFMA_MOPS_I8 x 512; 2*M*N*K = {ops}; "
+                     f"median over {len(sel(mfma['SQ_INSTS_MFMA']))} dispatches)"),
+                    ("mfma_busy_over_gui_active_per_simd",
+                     f"{med['SQ_VALU_MFMA_BUSY_CYCLES'] / N_SIMDS / gui:.3f}   (SQ_VALU_MFMA_BUSY_CYCLES per SIMD over "
+                     "GRBM_GUI_ACTIVE per XCD)"),
+                    ("valu_insts_per_mfma",
+                     f"{med['SQ_INSTS_VALU'] / med['SQ_INSTS_MFMA']:.2f}   (SQ_INSTS_VALU, which counts the MFMAs, over "
+                     "the 32x32x32 MFMA count)"),
+                    ("valu_active_over_gui_active_per_simd",
+                     f"{med['SQ_ACTIVE_INST_VALU'] * 4 / N_SIMDS / gui:.3f}   (SQ_ACTIVE_INST_VALU, quad-cycles, x 4 per "
+                     "SIMD over GRBM_GUI_ACTIVE per XCD)"),
+                    ("lds_wait_over_gui_active_per_simd",
+                     f"{med['SQ_WAIT_INST_LDS'] / N_SIMDS / gui:.3f}   (SQ_WAIT_INST_LDS per SIMD over GRBM_GUI_ACTIVE "
+                     "per XCD)"),
+                    ("raw", " ".join(f"{c}={med[c]:.0f}" for c in sorted(med))),
+                    ("sq_insts_mfma", f"{med['SQ_INSTS_MFMA']:.0f}")]
+        return label, avg, out
+
+    total = 0.0
+    for i in range(ng):
+        label, avg, out = stats_for(i)
+        total += avg
+        prefix = f"{label}." if label else ""
+        lines += [f"{prefix}{k}: {v}" for k, v in out]
+    if ng > 1:
+        lines.append(f"gemm_sum_avg_us: {total:.3f}")
+        if quant:
+            lines.append(f"quantize_avg_us: {statistics.mean(x for _, x in quant):.3f}")
+    lines.append(f"source_hash: {kernel_source_hash()}")
+    return "\n".join(lines) + "\n"
+
+
 def measure_ceilings():
     """Measured HBM-read and INT8-MFMA ceilings (libw4a8_ceiling.so): a plain
     16-byte streaming read of 1 GiB, and independent 32x32x32 int8 MFMA
@@ -809,7 +1024,18 @@ def main():
                     help="run only the flow-matching step workloads (for profiling their kernel)")
     ap.add_argument("--profile", default=None, metavar="WORKLOAD",
                     help="run one workload only, for rocprofv3: gate_up, qkv, down:M, layer:M")
+    ap.add_argument("--profile-commands", default=None, metavar="NAME",
+                    help="print the rocprofv3 commands of summary NAME (see --prof-dir)")
+    ap.add_argument("--summarize-profile", default=None, metavar="NAME",
+                    help="print summary NAME from the rocprofv3 CSV files under --prof-dir")
+    ap.add_argument("--prof-dir", default="gpurun_out/prof", help="rocprofv3 output root of the two options above")
     args = ap.parse_args()
+    if args.profile_commands:
+        print("\n".join(profile_commands(args.profile_commands, args.prof_dir)))
+        return
+    if args.summarize_profile:
+        sys.stdout.write(summarize_profile(args.summarize_profile, args.prof_dir))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(the layer would shard by output columns or by K).", file=sys.stderr)

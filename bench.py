@@ -751,8 +751,11 @@ def _csv_rows(run_dir: str, suffix: str):
 
 
 def _short_kernel(full: str) -> str:
-    """'void w4a8::(anonymous namespace)::smallm<1, 6, ...>(args)' -> 'smallm<1, 6, ...>'."""
-    name = full.split("(anonymous namespace)::")[-1]
+    """'void w4a8::(anonymous namespace)::smallm<1, 6, ...>(args)' -> 'smallm<1, 6, ...>':
+    the name up to its argument list, without return type and namespaces."""
+    name = full.replace("(anonymous namespace)::", "")
+    if name.startswith("void "):
+        name = name[5:]
     depth, out = 0, []
     for ch in name:
         if ch == "(" and depth == 0:
@@ -760,7 +763,13 @@ def _short_kernel(full: str) -> str:
         depth += ch == "<"
         depth -= ch == ">"
         out.append(ch)
-    return "".join(out)
+    name, depth, cut = "".join(out), 0, 0
+    for i, ch in enumerate(name):  # the last "::" outside template arguments
+        depth += ch == "<"
+        depth -= ch == ">"
+        if depth == 0 and name.startswith("::", i):
+            cut = i + 2
+    return name[cut:]
 
 
 def _is_gemm(kernel: str) -> bool:

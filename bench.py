@@ -1037,7 +1037,7 @@ def main():
                     help="print the rocprofv3 commands of summary NAME (see --prof-dir)")
     ap.add_argument("--summarize-profile", default=None, metavar="NAME",
                     help="print summary NAME from the rocprofv3 CSV files under --prof-dir")
-    ap.add_argument("--prof-dir", default="gpurun_out/prof", help="rocprofv3 output root of the two options above")
+    ap.add_argument("--prof-dir", default="prof", help="rocprofv3 output root of the two options above (default: ./prof)")
     args = ap.parse_args()
     if args.profile_commands:
         print("\n".join(profile_commands(args.profile_commands, args.prof_dir)))
